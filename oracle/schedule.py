@@ -1,0 +1,98 @@
+"""Simulated straggler schedule: per-mini-batch times, the terminal signal and
+the finished-mini-batch mask of one iteration (Alg. 2, the mini-batch loop;
+Lemma 1 and Thm 2 for the timing model).
+
+Each learner processes its N mini-batches in order.  The first learner to
+finish all of them broadcasts the terminal signal (Alg. 2, "broadcast terminal
+signals if n = N"); every learner keeps the mini-batches it finished by then and
+abandons the rest.  With the times of learner i written t[i, 0..m-1] and their
+running sums C[i, j], the signal time is T = min_i C[i, m-1] and learner i keeps
+mini-batches j with C[i, j] <= T (finished by the signal time, boundary
+included).  A learner that finished none keeps its first one (the step is
+undefined for zero finished mini-batches), which extends the iteration to that
+learner's first finish time.
+
+Delay models (rate convention for Exp, mean 1/rate, as in Remark 1 of App. A):
+
+* CONST:  D = 0
+* EXP:    D = -log(u) / rate
+* LOMAX:  D = u**(-1/shape) - 1   (so base 1 plus D is Pareto with scale 1)
+
+t[i, j] = s_i * (base + D) where s_i is ``slow_factor`` for the one slowed
+learner and 1 otherwise.  u comes from Philox word 0 at counter
+(step, i, j, 0) under key (seed, 1).  Scalar ``math.log`` / ``math.pow`` are
+used on purpose (the platform libm, one value at a time).
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import philox
+
+DELAY_CONST = 0
+DELAY_EXP = 1
+DELAY_LOMAX = 2
+
+
+@dataclass(frozen=True)
+class Delay:
+    kind: int = DELAY_EXP
+    base: float = 1.0
+    param: float = 1.0          # EXP: rate; LOMAX: shape
+    slow_learner: int = -1      # -1: nobody is slowed
+    slow_factor: float = 1.0
+
+
+def minibatch_time(seed: int, step: int, i: int, j: int, d: Delay) -> float:
+    """Wall time of learner i on mini-batch j of iteration ``step``."""
+    u = philox.u01(philox.word(seed, philox.PURPOSE_DELAY, step, i, j))
+    if d.kind == DELAY_CONST:
+        extra = 0.0
+    elif d.kind == DELAY_EXP:
+        extra = -math.log(u) / d.param
+    elif d.kind == DELAY_LOMAX:
+        extra = math.pow(u, -1.0 / d.param) - 1.0
+    else:
+        raise ValueError(f"unknown delay kind {d.kind}")
+    scale = d.slow_factor if i == d.slow_learner else 1.0
+    return scale * (d.base + extra)
+
+
+def sample_schedule(seed: int, step: int, n: int, m: int, d: Delay) -> dict:
+    """One iteration's schedule.
+
+    Returns a dict with ``times`` f64[n, m], ``finish`` f64[n, m] (running
+    sums), ``deadline`` T, ``counts`` int32[n], ``mask`` uint8[n, m] (1 =
+    finished), ``t_sync`` (time the slowest learner would need for all m, the
+    blocking baseline's iteration time) and ``t_step`` (this iteration's time
+    including any forced first mini-batch).
+    """
+    times = np.zeros((n, m), dtype=np.float64)
+    finish = np.zeros((n, m), dtype=np.float64)
+    for i in range(n):
+        running = 0.0
+        for j in range(m):
+            t = minibatch_time(seed, step, i, j, d)
+            running = running + t
+            times[i, j] = t
+            finish[i, j] = running
+    deadline = min(finish[i, m - 1] for i in range(n))
+    counts = np.zeros(n, dtype=np.int32)
+    mask = np.zeros((n, m), dtype=np.uint8)
+    for i in range(n):
+        done = 0
+        for j in range(m):
+            if finish[i, j] <= deadline:
+                done += 1
+        c = max(1, done)
+        counts[i] = c
+        for j in range(c):
+            mask[i, j] = 1
+    t_sync = max(finish[i, m - 1] for i in range(n))
+    t_step = max(deadline, max(finish[i, counts[i] - 1] for i in range(n)))
+    return dict(times=times, finish=finish, deadline=deadline, counts=counts, mask=mask,
+                t_sync=t_sync, t_step=t_step)

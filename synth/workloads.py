@@ -1,0 +1,77 @@
+"""The synthetic workloads: shapes, input distributions, delay models, mixing
+kinds and hyper-parameters.  Plain data; both the GPU-path tests/bench and the
+oracle read it, and each side maps the names to its own constants.
+
+The paper trains CNNs on CIFAR-10/100 (Sec. 6.1); neither the datasets nor the
+networks are available here, so flat parameter vectors sized like ResNet-18,
+ResNet-50 and VGG-16 with Gaussian per-mini-batch gradients stand in for them.
+Values never change the memory traffic of a step: the only data-dependent
+control flow is the finished-mini-batch mask.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field, replace
+
+# tensor streams of the input generator
+STREAM_X = 1
+STREAM_G = 2
+
+MIX_THEN_STEP = "mix_then_step"
+STEP_THEN_MIX = "step_then_mix"
+
+
+@dataclass(frozen=True)
+class DelaySpec:
+    kind: str = "exp"          # "const" | "exp" | "lomax"
+    base: float = 1.0
+    param: float = 1.0         # exp: rate; lomax: shape
+    slow_learner: int = -1
+    slow_factor: float = 1.0
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    n: int
+    m: int
+    P: int
+    mixing: str                # "uniform" | "ring" | "matcha"
+    order: str
+    delay: DelaySpec
+    lr: float
+    momentum: float
+    steps: int
+    seed: int = 0
+    x_std: float = 1.0
+    g_std: float = math.sqrt(1e-3)   # N(0, 1e-3) read as variance 1e-3
+    matcha_degree: int = 3
+    notes: str = ""
+    extra: dict = field(default_factory=dict)
+
+    def with_P(self, P: int) -> "Workload":
+        return replace(self, P=P)
+
+    def alg_bytes(self, sum_counts: int) -> int:
+        """Algorithmic HBM bytes of one fused step: the finished gradient rows
+        once, X and V read once and written once."""
+        return 4 * self.P * (sum_counts + 4 * self.n)
+
+
+TINY = Workload("tiny_n4_m4_P10k_allreduce", 4, 4, 10_000, "uniform", STEP_THEN_MIX,
+                DelaySpec("exp", 1.0, 1.0), 0.1, 0.9, 10)
+RESNET18_RING = Workload("resnet18_n8_m8_P11.2M_ring", 8, 8, 11_200_000, "ring", MIX_THEN_STEP,
+                         DelaySpec("exp", 1.0, 1.0, slow_learner=7, slow_factor=3.0), 0.1, 0.9, 50)
+RESNET50_MATCHA = Workload("resnet50_n16_m4_P23.5M_matcha", 16, 4, 23_500_000, "matcha",
+                           MIX_THEN_STEP, DelaySpec("exp", 1.0, 0.5), 0.1, 0.9, 50)
+VGG16_ALLREDUCE = Workload("vgg16_n8_m16_P138M_allreduce", 8, 16, 138_000_000, "uniform",
+                           STEP_THEN_MIX, DelaySpec("lomax", 1.0, 1.5), 0.05, 0.9, 20)
+
+WORKLOADS = {w.name: w for w in (TINY, RESNET18_RING, RESNET50_MATCHA, VGG16_ALLREDUCE)}
+ALIASES = {"tiny": TINY.name, "resnet18": RESNET18_RING.name, "resnet50": RESNET50_MATCHA.name,
+           "vgg16": VGG16_ALLREDUCE.name}
+
+
+def get(name: str) -> Workload:
+    return WORKLOADS[ALIASES.get(name, name)]

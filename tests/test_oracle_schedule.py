@@ -1,0 +1,102 @@
+"""Pins for the simulated schedule: Lemma 1 / Thm 2 closed forms (App. A and B),
+the Lomax tail, and the structural invariants of the mask."""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle import schedule
+from oracle.schedule import DELAY_CONST, DELAY_EXP, DELAY_LOMAX, Delay
+
+
+def _paper_sync_sum(n, lam):
+    # App. B closed form: (n / lam) * sum_k C(n-1, k) (-1)^k / (k + 1)^2
+    return (n / lam) * sum(math.comb(n - 1, k) * (-1) ** k / (k + 1) ** 2 for k in range(n))
+
+
+@pytest.mark.parametrize("n", [2, 4, 8, 10, 16])
+def test_paper_sum_is_harmonic_number(n):
+    # E[max of n Exp(lam)] is H_n / lam (textbook); the paper's sum must agree
+    H = sum(1.0 / k for k in range(1, n + 1))
+    assert _paper_sync_sum(n, 1.0) == pytest.approx(H, rel=1e-9)
+
+
+@pytest.mark.parametrize("n,lam", [(4, 1.0), (10, 0.5)])
+def test_thm2_expected_iteration_times(n, lam):
+    # One mini-batch per learner and no constant part: the terminal signal
+    # comes at the minimum of n Exp(lam) times, E = 1 / (n lam) (Thm 2,
+    # App. A); the blocking baseline waits for the maximum (App. B).
+    d = Delay(DELAY_EXP, base=0.0, param=lam)
+    draws = 6000
+    T = np.empty(draws)
+    S = np.empty(draws)
+    for k in range(draws):
+        s = schedule.sample_schedule(3, k, n, 1, d)
+        T[k] = s["deadline"]
+        S[k] = s["t_sync"]
+    mean_min, sd_min = 1.0 / (n * lam), 1.0 / (n * lam)  # min is Exp(n lam)
+    z = (T.mean() - mean_min) / (sd_min / math.sqrt(draws))
+    assert abs(z) < 4.0
+    var_max = sum(1.0 / (k * lam) ** 2 for k in range(1, n + 1))
+    z = (S.mean() - _paper_sync_sum(n, lam)) / math.sqrt(var_max / draws)
+    assert abs(z) < 4.0
+
+
+def test_lomax_tail():
+    # base 0: D itself, P(D > x) = (1 + x)^-shape
+    d = Delay(DELAY_LOMAX, base=0.0, param=1.5)
+    xs = np.array([schedule.minibatch_time(5, 0, 0, j, d) for j in range(20000)])
+    for x in (0.5, 1.0, 3.0, 10.0):
+        p = (1.0 + x) ** -1.5
+        emp = (xs > x).mean()
+        assert abs(emp - p) < 4.0 * math.sqrt(p * (1 - p) / xs.size)
+
+
+def test_exp_mean_and_scale():
+    d = Delay(DELAY_EXP, base=1.0, param=0.5, slow_learner=1, slow_factor=3.0)
+    t0 = np.array([schedule.minibatch_time(9, k, 0, 0, d) for k in range(5000)])
+    t1 = np.array([schedule.minibatch_time(9, k, 1, 0, d) for k in range(5000)])
+    assert t0.min() > 1.0
+    assert abs(t0.mean() - 3.0) < 4 * 2.0 / math.sqrt(5000)  # 1 + mean 1/0.5
+    assert abs(t1.mean() - 9.0) < 4 * 6.0 / math.sqrt(5000)  # slowed x3
+
+
+@pytest.mark.parametrize("kind", [DELAY_EXP, DELAY_LOMAX])
+def test_mask_invariants(kind):
+    d = Delay(kind, 1.0, 1.0 if kind == DELAY_EXP else 1.5, slow_learner=2, slow_factor=3.0)
+    for step in range(40):
+        s = schedule.sample_schedule(0, step, 6, 5, d)
+        mask, counts = s["mask"], s["counts"]
+        assert counts.min() >= 1 and counts.max() == 5  # the signaller finished all
+        for i in range(6):
+            assert list(mask[i]) == [1] * counts[i] + [0] * (5 - counts[i])
+            # finished mini-batches end no later than the deadline, unless forced
+            if counts[i] > 1 or s["finish"][i, 0] <= s["deadline"]:
+                assert s["finish"][i, counts[i] - 1] <= s["deadline"]
+            if counts[i] < 5:
+                assert s["finish"][i, counts[i]] > s["deadline"]
+        assert s["deadline"] == s["finish"][:, -1].min()
+        assert s["t_sync"] == s["finish"][:, -1].max()
+        assert s["t_step"] >= s["deadline"]
+
+
+def test_const_delay_gives_full_mask():
+    s = schedule.sample_schedule(0, 0, 5, 7, Delay(DELAY_CONST, base=1.0))
+    assert s["mask"].all() and (s["counts"] == 7).all()
+
+
+def test_huge_straggler_keeps_one_minibatch():
+    d = Delay(DELAY_EXP, 1.0, 1.0, slow_learner=0, slow_factor=1e9)
+    s = schedule.sample_schedule(0, 0, 4, 8, d)
+    assert s["counts"][0] == 1
+    assert s["t_step"] == s["finish"][0, 0] > s["deadline"]
+
+
+def test_deterministic_in_seed_and_step():
+    d = Delay(DELAY_EXP, 1.0, 1.0)
+    a = schedule.sample_schedule(11, 4, 4, 4, d)
+    b = schedule.sample_schedule(11, 4, 4, 4, d)
+    c = schedule.sample_schedule(11, 5, 4, 4, d)
+    assert np.array_equal(a["times"], b["times"])
+    assert not np.array_equal(a["times"], c["times"])
