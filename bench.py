@@ -1,0 +1,150 @@
+"""Throughput of the fused Non-blocking SGD step on one MI355X.
+
+One "step" is one whole iteration of the hot path: the simulated schedule
+(finished-mini-batch mask) and mixing matrix on the host, then the fused
+``nbsgd_step`` kernel (accumulate finished gradients, momentum, mix, update)
+over replicas, momentum buffers and per-mini-batch gradients resident in HBM.
+
+Prints one JSON line:
+  value      learner-parameter updates per second, n * P * steps / wall time
+             between two device synchronisations around the timed steps
+  roofline   the fused kernel's achieved HBM bandwidth: algorithmic bytes
+             4 * P * (sum of finished counts + 4 n) per launch, summed over the
+             timed launches, over the summed kernel durations from HIP events
+             recorded on the launch stream; against the 8 TB/s HBM3E peak
+  cpu_baseline  the CPU oracle (fp64 NumPy, one thread) on a bounded column
+             window of the same workload, scaled to the same unit
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "learner-param updates/sec and achieved HBM GB/s (% peak) for fused nbsgd_step"
+UNIT = "learner-param updates/s"
+
+
+def cpu_baseline(wl, budget_s: float = 15.0, cols: int = 1 << 19):
+    """The oracle on columns [0, cols) of the workload, one thread, about
+    ``budget_s`` seconds; returns learner-param updates per second."""
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    from tests._util import ORACLE_ORDER, OracleMixer, oracle_delay, window_inputs
+
+    cols = min(cols, wl.P)
+    X0, G = window_inputs(wl, np.arange(cols))
+    X = X0.astype(np.float64)
+    V = np.zeros_like(X)
+    mixer, d = OracleMixer(wl), oracle_delay(wl)
+    lr, mu = float(np.float32(wl.lr)), float(np.float32(wl.momentum))
+    steps = 0
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        while True:
+            s = oracle.schedule.sample_schedule(wl.seed, steps, wl.n, wl.m, d)
+            X, V = oracle.step.step(X, V, G, s["mask"], mixer.w(steps), lr, mu,
+                                    ORACLE_ORDER[wl.order])
+            steps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s:
+                break
+    return {"value": wl.n * cols * steps / el, "unit": UNIT, "cores": 1, "kind": "oracle",
+            "sample": f"{wl.name}: columns [0, {cols}) of P={wl.P}, {steps} steps in {el:.1f} s "
+                      f"(fp64 NumPy, 1 thread; the step is column-separable so per-column cost "
+                      f"is constant)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="resnet18")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the simulated learners are replicas in one "
+              f"GPU's HBM and this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2211_00889_amd import runner
+    from synth import workloads
+
+    wl = workloads.get(args.workload)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    r = runner.StepRunner(wl, dev)
+    stream = torch.cuda.current_stream(dev)
+
+    for k in range(args.warmup):
+        mask, counts, _, W = r.plan(k)
+        r.launch(mask, W)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    sum_counts = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        mask, counts, _, W = r.plan(args.warmup + i)
+        starts[i].record(stream)
+        r.launch(mask, W)
+        ends[i].record(stream)
+        sum_counts.append(int(counts.sum()))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    kern_ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+    alg_bytes = np.array([wl.alg_bytes(c) for c in sum_counts], dtype=np.float64)
+    achieved = alg_bytes.sum() / (kern_ms.sum() * 1e-3) / 1e9
+    value = wl.n * wl.P * K / wall
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": UNIT,
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded SplitMix64 Irwin-Hall normals: X ~ N(0, 1), G ~ N(0, 1e-3))",
+        "config": {"workload": wl.name, "n_learners": wl.n, "minibatches": wl.m, "P": wl.P,
+                   "mixing": wl.mixing, "order": wl.order, "delay": wl.delay.kind,
+                   "lr": wl.lr, "momentum": wl.momentum,
+                   "mean_finished_per_step": float(np.mean(sum_counts))},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "kernel": "k_step", "kernel_ms_mean": float(kern_ms.mean()),
+                     "kernel_ms_median": float(np.median(kern_ms)),
+                     "alg_bytes_per_launch_mean": float(alg_bytes.mean())},
+    }
+    del r
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

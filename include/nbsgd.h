@@ -1,0 +1,204 @@
+/*
+ * nbsgd.h - C ABI of libnbsgd, the MI355X (gfx950) hot path of Non-blocking SGD
+ * (He & Dube, "Accelerating Parallel Stochastic Gradient Descent via
+ * Non-blocking Mini-batches", arXiv 2211.00889).
+ *
+ * n learners are simulated as parameter replicas resident in one GPU's HBM.
+ * One iteration (Alg. 2) is:
+ *   1. every learner processes its mini-batches in order until the fastest
+ *      learner, having finished all m, broadcasts the terminal signal; the
+ *      unfinished mini-batches are abandoned            -> nbsgd_sample_mask
+ *   2. each learner averages the gradients of its finished mini-batches
+ *                                                        -> nbsgd_accumulate
+ *   3. models are averaged through a doubly stochastic mixing matrix W
+ *      (ring all-reduce, D-PSGD ring gossip or MATCHA)   -> nbsgd_mix
+ *   4. each learner takes one local step with learning rate lr * c_i / m,
+ *      here with heavy-ball momentum                     -> nbsgd_update
+ * nbsgd_step does 2-4 in one pass over HBM.
+ *
+ * Notation: n learners (the paper's P), m mini-batches per learner per
+ * iteration (the paper's N), P parameters per replica (the paper's d),
+ * c_i finished mini-batches of learner i (the paper's n_{k,i}).
+ *
+ * Conventions for every call:
+ *   - returns nbsgd_status; NBSGD_OK is 0.  On error nothing is enqueued and
+ *     nbsgd_last_error() (thread-local) describes the first failed check.
+ *   - device buffers are fp32, contiguous, row-major, caller-owned (typically
+ *     torch.empty(..., device="cuda")); the library never retains or frees a
+ *     pointer.  Base pointers must be 16-byte aligned (NBSGD_E_ALIGN).
+ *   - host arrays (mask, counts, W) are read completely before the call
+ *     returns; the caller may reuse them at once.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Kernels are enqueued asynchronously; device faults surface at the
+ *     caller's next synchronisation.  No hot call allocates or synchronises.
+ *   - limits: 1 <= n <= NBSGD_MAX_LEARNERS, 1 <= m <= NBSGD_MAX_MINIBATCHES
+ *     (NBSGD_E_UNSUPPORTED beyond); P >= 0, P == 0 is a valid empty call.
+ *   - all functions are reentrant; calls on one stream execute in order.
+ */
+#ifndef NBSGD_H
+#define NBSGD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define NBSGD_MAX_LEARNERS 16
+#define NBSGD_MAX_MINIBATCHES 64
+
+typedef enum {
+  NBSGD_OK = 0,
+  NBSGD_E_ARG = 1,         /* null pointer, bad enum, overlapping buffers */
+  NBSGD_E_SHAPE = 2,       /* negative or inconsistent sizes */
+  NBSGD_E_ALIGN = 3,       /* device base pointer not 16-byte aligned */
+  NBSGD_E_MASK = 4,        /* a learner with no finished mini-batch */
+  NBSGD_E_W = 5,           /* W not finite, negative, or not doubly stochastic */
+  NBSGD_E_HIP = 6,         /* a HIP runtime call or kernel launch failed */
+  NBSGD_E_UNSUPPORTED = 7  /* n or m beyond the compiled limits */
+} nbsgd_status;
+
+/* Order of the averaging and the local step.  MIX_THEN_STEP averages the
+ * pre-step models and subtracts each learner's own step (Alg. 2, averaging
+ * then update).  STEP_THEN_MIX steps first and averages the stepped models
+ * (Eq. 4-5 ring all-reduce, Eq. 6 D-PSGD, Alg. 3). */
+typedef enum { NBSGD_MIX_THEN_STEP = 0, NBSGD_STEP_THEN_MIX = 1 } nbsgd_order;
+
+/* Per-mini-batch time model: t = s_i * (base + D), s_i = slow_factor for
+ * learner slow_learner (-1: none) and 1 otherwise.
+ *   CONST: D = 0
+ *   EXP:   D ~ Exp(rate = param), mean 1/param (App. A, Remark 1)
+ *   LOMAX: D = Pareto type II with shape param, so base 1 + D is Pareto with
+ *          scale 1 (heavy-tailed stragglers)                                  */
+typedef enum { NBSGD_DELAY_CONST = 0, NBSGD_DELAY_EXP = 1, NBSGD_DELAY_LOMAX = 2 } nbsgd_delay_kind;
+
+typedef struct {
+  int32_t kind;        /* nbsgd_delay_kind */
+  double base;         /* >= 0 */
+  double param;        /* EXP: rate > 0; LOMAX: shape > 0; CONST: ignored */
+  int32_t slow_learner;
+  double slow_factor;  /* > 0 */
+} nbsgd_delay;
+
+/* ---------------------------------------------------------------- schedule
+ * Simulated terminal signal of one iteration (Alg. 2 mini-batch loop; Lemma 1).
+ * Mini-batch j of learner i at iteration `step` takes t[i][j] (delay model
+ * above; the uniform variate is Philox4x64-10 word 0 at counter
+ * (step, i, j, 0) under key (seed, 1), mapped to ((w >> 12) + 0.5) * 2^-52).
+ * With C[i][j] the running sum of t[i][0..j] (fp64, j ascending), the signal
+ * comes at T = min_i C[i][m-1]; learner i finished c_i = max(1, #{j :
+ * C[i][j] <= T}) mini-batches, its first c_i.
+ * Outputs (host, caller-owned):
+ *   mask   uint8[n*m], row-major: mask[i*m+j] = 1 iff j < c_i
+ *   counts int32[n]:   c_i
+ *   times  double[n*m] (nullable): t[i][j]
+ *   timing double[3]   (nullable): {T, T_sync = max_i C[i][m-1] (the blocking
+ *          iteration time), T_step = max(T, max_i C[i][c_i-1])}
+ * Errors: NBSGD_E_ARG (null mask/counts/d, bad kind or non-positive param),
+ *         NBSGD_E_SHAPE, NBSGD_E_UNSUPPORTED.                                  */
+nbsgd_status nbsgd_sample_mask(uint64_t seed, uint64_t step, int32_t n, int32_t m,
+                               const nbsgd_delay *d, uint8_t *mask, int32_t *counts,
+                               double *times, double *timing);
+
+/* ------------------------------------------------------------- accumulate
+ * Accumulated gradient of the finished mini-batches (Alg. 2 mini-batch loop;
+ * Sec. 3.2 "compute gradients"), normalised by the finished count:
+ *   Gbar[i][:] = (1 / c_i) * sum_{j : mask[i*m+j] != 0} G[i][j][:]
+ * G     device fp32 [n][m][P] (only finished rows are read)
+ * mask  host uint8 [n*m], any pattern; c_i = number of nonzero entries >= 1
+ * Gbar  device fp32 [n][P], written; must not overlap G
+ * Errors: NBSGD_E_ARG, NBSGD_E_SHAPE, NBSGD_E_ALIGN, NBSGD_E_MASK,
+ *         NBSGD_E_UNSUPPORTED, NBSGD_E_HIP.                                    */
+nbsgd_status nbsgd_accumulate(const float *G, const uint8_t *mask, int32_t n, int32_t m,
+                              int64_t P, float *Gbar, void *stream);
+
+/* -------------------------------------------------------------------- mix
+ * Neighbourhood averaging (Alg. 2 averaging step; Eq. 6):
+ *   Y[i][:] = sum_p W[i*n+p] * X[p][:]
+ * X, Y  device fp32 [n][P]; Y == X (in place) is allowed, partial overlap is
+ *       not (NBSGD_E_ARG)
+ * W     host fp32 [n*n], row-major; entries finite and >= 0, every row and
+ *       column sum within 1e-5 of 1 (NBSGD_E_W).  Zero entries are skipped; a
+ *       W whose entries are all equal (ring all-reduce, J/n) takes a path that
+ *       sums once and scales, so every row of Y is bitwise identical.
+ * Errors: NBSGD_E_ARG, NBSGD_E_SHAPE, NBSGD_E_ALIGN, NBSGD_E_W,
+ *         NBSGD_E_UNSUPPORTED, NBSGD_E_HIP.                                    */
+nbsgd_status nbsgd_mix(const float *X, const float *W, int32_t n, int64_t P, float *Y,
+                       void *stream);
+
+/* ----------------------------------------------------------------- update
+ * Local step with the finished-fraction learning rate (Sec. 3.2 "adjust
+ * learning rate" and "gradient update") and heavy-ball momentum:
+ *   eta_i = lr * counts[i] / m   (fp64, rounded once to fp32)
+ *   V[i] = momentum * V[i] + Gbar[i];   X[i] = X[i] - eta_i * V[i]
+ * X, V  device fp32 [n][P], updated in place
+ * Gbar  device fp32 [n][P] (from nbsgd_accumulate)
+ * counts host int32 [n], 1 <= counts[i] <= m
+ * Errors: NBSGD_E_ARG, NBSGD_E_SHAPE, NBSGD_E_ALIGN, NBSGD_E_MASK (a count
+ *         outside [1, m]), NBSGD_E_UNSUPPORTED, NBSGD_E_HIP.                  */
+nbsgd_status nbsgd_update(float *X, float *V, const float *Gbar, const int32_t *counts, int32_t n,
+                          int32_t m, int64_t P, float lr, float momentum, void *stream);
+
+/* ------------------------------------------------------------------- step
+ * One whole Non-blocking iteration after the schedule (Alg. 2), fused so X, V
+ * and the finished rows of G each cross HBM once:
+ *   g_i   = (1/c_i) sum_{finished j} G[i][j]     eta_i = lr * c_i / m
+ *   V[i]  = momentum * V[i] + g_i
+ *   MIX_THEN_STEP: X[i] = sum_p W[i*n+p] X[p] - eta_i V[i]
+ *   STEP_THEN_MIX: X[i] = sum_p W[i*n+p] (X[p] - eta_p V[p])
+ * Equal, up to fp32 rounding, to accumulate + mix + update (MIX_THEN_STEP) or
+ * accumulate + update + mix (STEP_THEN_MIX).
+ * X, V  device fp32 [n][P], updated in place; G device fp32 [n][m][P], must
+ *       not overlap X or V; X and V must not overlap.
+ * mask, W as above; order is an nbsgd_order.
+ * Errors: NBSGD_E_ARG, NBSGD_E_SHAPE, NBSGD_E_ALIGN, NBSGD_E_MASK, NBSGD_E_W,
+ *         NBSGD_E_UNSUPPORTED, NBSGD_E_HIP.                                    */
+nbsgd_status nbsgd_step(float *X, float *V, const float *G, const uint8_t *mask, const float *W,
+                        int32_t n, int32_t m, int64_t P, float lr, float momentum, int32_t order,
+                        void *stream);
+
+/* ------------------------------------------------------- mixing matrices
+ * Host builders, W fp32 [n*n] row-major, caller-owned.
+ * nbsgd_w_allreduce: every entry 1/n (ring all-reduce averages all replicas,
+ *   Eq. 4-5).
+ * nbsgd_w_ring: D-PSGD on a ring (Eq. 6): W[i][i] = W[i][i+-1 mod n] = 1/3;
+ *   n = 2 gives all entries 1/2, n = 1 gives [1].
+ * Errors: NBSGD_E_ARG (null W), NBSGD_E_SHAPE, NBSGD_E_UNSUPPORTED.          */
+nbsgd_status nbsgd_w_allreduce(int32_t n, float *W);
+nbsgd_status nbsgd_w_ring(int32_t n, float *W);
+
+/* MATCHA with communication budget 1/2 (Sec. 6.1): a random `degree`-regular
+ * simple connected base graph on n nodes (pairing model; half-edge shuffle by
+ * Fisher-Yates from the top with Philox4x64-10 word 0 at counter
+ * (attempt, position, 0, 0) under key (seed, 2) mapped to [0, t] by
+ * floor(w * (t+1) / 2^64); rejected and redrawn on a loop, a repeated edge or
+ * a disconnected graph), split into matchings by greedy edge colouring in
+ * lexicographic edge order.  At iteration `step` matching q is active iff the
+ * top bit of Philox word 0 at counter (step, q, 0, 0) under key (seed, 3) is
+ * 0, and W = I - alpha * sum_{active q} L_q, L_q the Laplacian of matching q,
+ * alpha = 1 / (degree + 1).
+ * nbsgd_matcha_create: builds the graph; *out is owned by the caller and
+ *   released with nbsgd_matcha_destroy.  Errors: NBSGD_E_ARG, NBSGD_E_SHAPE
+ *   (no such regular graph), NBSGD_E_UNSUPPORTED.
+ * nbsgd_matcha_w: W of iteration `step`; n_active (nullable) receives the
+ *   number of active matchings.
+ * nbsgd_matcha_matchings: edges_uvq int32[3*E] as (u, v, matching) with u < v
+ *   in lexicographic order (nullable to query sizes), *E edges, *M matchings.
+ */
+typedef struct nbsgd_matcha nbsgd_matcha;
+nbsgd_status nbsgd_matcha_create(uint64_t seed, int32_t n, int32_t degree, nbsgd_matcha **out);
+nbsgd_status nbsgd_matcha_w(const nbsgd_matcha *g, uint64_t step, float *W, int32_t *n_active);
+nbsgd_status nbsgd_matcha_matchings(const nbsgd_matcha *g, int32_t *edges_uvq, int32_t *E,
+                                    int32_t *M);
+void nbsgd_matcha_destroy(nbsgd_matcha *g);
+
+/* ---------------------------------------------------------------- errors
+ * Text of the last failed check or HIP error on the calling thread ("" if
+ * none).  The pointer stays valid until the next nbsgd call on the thread. */
+const char *nbsgd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NBSGD_H */

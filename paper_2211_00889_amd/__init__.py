@@ -1,0 +1,23 @@
+"""MI355X (gfx950) hot path of Non-blocking SGD (He & Dube, arXiv 2211.00889).
+
+The product is the C-ABI library ``libnbsgd.so`` (declared in ``include/nbsgd.h``);
+``_lib`` is its ctypes binding with the same names.
+"""
+
+from ._lib import (  # noqa: F401
+    DELAY_CONST,
+    DELAY_EXP,
+    DELAY_LOMAX,
+    MIX_THEN_STEP,
+    STEP_THEN_MIX,
+    Matcha,
+    NbsgdError,
+    accumulate,
+    load,
+    mix,
+    sample_mask,
+    step,
+    update,
+    w_allreduce,
+    w_ring,
+)

@@ -1,0 +1,215 @@
+"""ctypes binding of libnbsgd.so: argument marshalling only.
+
+Every computation happens in the library (host C++ for the schedule and the
+mixing matrices, gfx950 kernels for the step).  Device arrays are PyTorch CUDA
+tensors used as plain device memory; the stream defaults to torch's current
+stream on the tensor's device.  A missing library raises at import time of the
+first call, never falls back to anything else.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libnbsgd.so")
+
+OK, E_ARG, E_SHAPE, E_ALIGN, E_MASK, E_W, E_HIP, E_UNSUPPORTED = range(8)
+MIX_THEN_STEP, STEP_THEN_MIX = 0, 1
+DELAY_CONST, DELAY_EXP, DELAY_LOMAX = 0, 1, 2
+MAX_LEARNERS, MAX_MINIBATCHES = 16, 64
+
+EXPORTS = ("nbsgd_sample_mask", "nbsgd_accumulate", "nbsgd_mix", "nbsgd_update", "nbsgd_step",
+           "nbsgd_w_allreduce", "nbsgd_w_ring", "nbsgd_matcha_create", "nbsgd_matcha_w",
+           "nbsgd_matcha_matchings", "nbsgd_matcha_destroy", "nbsgd_last_error")
+
+
+class NbsgdError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"nbsgd status {status}: {message}")
+        self.status = status
+
+
+class Delay(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("base", ctypes.c_double), ("param", ctypes.c_double),
+                ("slow_learner", ctypes.c_int32), ("slow_factor", ctypes.c_double)]
+
+
+_c_void_p, _i32, _i64, _u64, _f32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                     ctypes.c_uint64, ctypes.c_float)
+_lib = None
+
+
+def load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    sig = {
+        "nbsgd_sample_mask": [_u64, _u64, _i32, _i32, ctypes.POINTER(Delay), _c_void_p, _c_void_p,
+                              _c_void_p, _c_void_p],
+        "nbsgd_accumulate": [_c_void_p, _c_void_p, _i32, _i32, _i64, _c_void_p, _c_void_p],
+        "nbsgd_mix": [_c_void_p, _c_void_p, _i32, _i64, _c_void_p, _c_void_p],
+        "nbsgd_update": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i64, _f32, _f32,
+                         _c_void_p],
+        "nbsgd_step": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i64,
+                       _f32, _f32, _i32, _c_void_p],
+        "nbsgd_w_allreduce": [_i32, _c_void_p],
+        "nbsgd_w_ring": [_i32, _c_void_p],
+        "nbsgd_matcha_create": [_u64, _i32, _i32, ctypes.POINTER(_c_void_p)],
+        "nbsgd_matcha_w": [_c_void_p, _u64, _c_void_p, _c_void_p],
+        "nbsgd_matcha_matchings": [_c_void_p, _c_void_p, _c_void_p, _c_void_p],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.nbsgd_matcha_destroy.argtypes = [_c_void_p]
+    lib.nbsgd_matcha_destroy.restype = None
+    lib.nbsgd_last_error.argtypes = []
+    lib.nbsgd_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != OK:
+        raise NbsgdError(status, load().nbsgd_last_error().decode())
+
+
+def _host_ptr(a: np.ndarray):
+    return a.ctypes.data_as(_c_void_p)
+
+
+def _dev(t, name):
+    import torch
+
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA tensor")
+    if t.dtype != torch.float32 or not t.is_contiguous():
+        raise TypeError(f"{name} must be contiguous float32")
+    return _c_void_p(t.data_ptr())
+
+
+def _stream(t, stream):
+    import torch
+
+    if stream is None:
+        return _c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return _c_void_p(stream.cuda_stream)
+    return _c_void_p(int(stream))
+
+
+def _u8(a, shape):
+    a = np.ascontiguousarray(np.asarray(a), dtype=np.uint8)
+    if a.shape != shape:
+        raise ValueError(f"expected shape {shape}, got {a.shape}")
+    return a
+
+
+def _w32(W, n):
+    W = np.ascontiguousarray(np.asarray(W), dtype=np.float32)
+    if W.shape != (n, n):
+        raise ValueError(f"W must be {n}x{n}")
+    return W
+
+
+# ------------------------------------------------------------------ host calls
+def sample_mask(seed: int, step: int, n: int, m: int, kind: int, base: float = 1.0,
+                param: float = 1.0, slow_learner: int = -1, slow_factor: float = 1.0):
+    """Returns (mask uint8[n, m], counts int32[n], times f64[n, m], timing f64[3])."""
+    d = Delay(kind, base, param, slow_learner, slow_factor)
+    mask = np.zeros((max(n, 0), max(m, 0)), np.uint8)
+    counts = np.zeros(max(n, 0), np.int32)
+    times = np.zeros((max(n, 0), max(m, 0)), np.float64)
+    timing = np.zeros(3, np.float64)
+    _check(load().nbsgd_sample_mask(seed, step, n, m, ctypes.byref(d), _host_ptr(mask),
+                                    _host_ptr(counts), _host_ptr(times), _host_ptr(timing)))
+    return mask, counts, times, timing
+
+
+def w_allreduce(n: int) -> np.ndarray:
+    W = np.zeros((max(n, 0), max(n, 0)), np.float32)
+    _check(load().nbsgd_w_allreduce(n, _host_ptr(W)))
+    return W
+
+
+def w_ring(n: int) -> np.ndarray:
+    W = np.zeros((max(n, 0), max(n, 0)), np.float32)
+    _check(load().nbsgd_w_ring(n, _host_ptr(W)))
+    return W
+
+
+class Matcha:
+    """Owner of an nbsgd_matcha handle."""
+
+    def __init__(self, seed: int, n: int, degree: int):
+        self.n = n
+        h = _c_void_p()
+        _check(load().nbsgd_matcha_create(seed, n, degree, ctypes.byref(h)))
+        self._h = h
+
+    def w(self, step: int):
+        W = np.zeros((self.n, self.n), np.float32)
+        active = ctypes.c_int32(0)
+        _check(load().nbsgd_matcha_w(self._h, step, _host_ptr(W), ctypes.byref(active)))
+        return W, active.value
+
+    def matchings(self):
+        E, M = ctypes.c_int32(0), ctypes.c_int32(0)
+        _check(load().nbsgd_matcha_matchings(self._h, None, ctypes.byref(E), ctypes.byref(M)))
+        buf = np.zeros((E.value, 3), np.int32)
+        _check(load().nbsgd_matcha_matchings(self._h, _host_ptr(buf), ctypes.byref(E),
+                                             ctypes.byref(M)))
+        return buf, M.value
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load().nbsgd_matcha_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        self.close()
+
+
+# ---------------------------------------------------------------- device calls
+def accumulate(G, mask, Gbar, stream=None):
+    n, m, P = G.shape
+    mask = _u8(mask, (n, m))
+    if tuple(Gbar.shape) != (n, P):
+        raise ValueError("Gbar must be [n, P]")
+    _check(load().nbsgd_accumulate(_dev(G, "G"), _host_ptr(mask), n, m, P, _dev(Gbar, "Gbar"),
+                                   _stream(G, stream)))
+
+
+def mix(X, W, Y, stream=None):
+    n, P = X.shape
+    W = _w32(W, n)
+    if tuple(Y.shape) != (n, P):
+        raise ValueError("Y must be [n, P]")
+    _check(load().nbsgd_mix(_dev(X, "X"), _host_ptr(W), n, P, _dev(Y, "Y"), _stream(X, stream)))
+
+
+def update(X, V, Gbar, counts, m: int, lr: float, momentum: float, stream=None):
+    n, P = X.shape
+    counts = np.ascontiguousarray(np.asarray(counts), dtype=np.int32)
+    if counts.shape != (n,) or tuple(V.shape) != (n, P) or tuple(Gbar.shape) != (n, P):
+        raise ValueError("shape mismatch")
+    _check(load().nbsgd_update(_dev(X, "X"), _dev(V, "V"), _dev(Gbar, "Gbar"), _host_ptr(counts),
+                               n, m, P, lr, momentum, _stream(X, stream)))
+
+
+def step(X, V, G, mask, W, lr: float, momentum: float, order: int, stream=None):
+    n, m, P = G.shape
+    if tuple(X.shape) != (n, P) or tuple(V.shape) != (n, P):
+        raise ValueError("X and V must be [n, P] with G [n, m, P]")
+    mask = _u8(mask, (n, m))
+    W = _w32(W, n)
+    _check(load().nbsgd_step(_dev(X, "X"), _dev(V, "V"), _dev(G, "G"), _host_ptr(mask),
+                             _host_ptr(W), n, m, P, lr, momentum, order, _stream(X, stream)))

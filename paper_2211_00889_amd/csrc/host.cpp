@@ -1,0 +1,324 @@
+// Host half of libnbsgd: the simulated straggler schedule, mixing-matrix
+// builders (uniform, ring, MATCHA), argument checks and the thread-local error
+// text.  Built with g++ -ffp-contract=off so every fp64 operation of the
+// schedule is a single IEEE operation in source order and log/pow are the
+// platform libm's.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <set>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "internal.h"
+
+namespace nbsgd {
+
+namespace {
+thread_local std::string g_error;
+}  // namespace
+
+nbsgd_status fail(nbsgd_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return st;
+}
+
+void clear_error() { g_error.clear(); }
+
+nbsgd_status check_nm(int32_t n, int32_t m) {
+  if (n < 1 || m < 1) return fail(NBSGD_E_SHAPE, "n=%d and m=%d must be >= 1", n, m);
+  if (n > NBSGD_MAX_LEARNERS)
+    return fail(NBSGD_E_UNSUPPORTED, "n=%d exceeds NBSGD_MAX_LEARNERS=%d", n, NBSGD_MAX_LEARNERS);
+  if (m > NBSGD_MAX_MINIBATCHES)
+    return fail(NBSGD_E_UNSUPPORTED, "m=%d exceeds NBSGD_MAX_MINIBATCHES=%d", m,
+                NBSGD_MAX_MINIBATCHES);
+  return NBSGD_OK;
+}
+
+nbsgd_status check_w(const float* W, int32_t n) {
+  if (W == nullptr) return fail(NBSGD_E_ARG, "W is null");
+  for (int32_t i = 0; i < n; ++i) {
+    double row = 0.0, col = 0.0;
+    for (int32_t p = 0; p < n; ++p) {
+      const float a = W[i * n + p];
+      if (!isfinite(a) || a < 0.0f)
+        return fail(NBSGD_E_W, "W[%d][%d]=%g is negative or not finite", i, p, (double)a);
+      row += a;
+      col += W[p * n + i];
+    }
+    if (fabs(row - 1.0) > 1e-5) return fail(NBSGD_E_W, "row %d of W sums to %.9g", i, row);
+    if (fabs(col - 1.0) > 1e-5) return fail(NBSGD_E_W, "column %d of W sums to %.9g", i, col);
+  }
+  return NBSGD_OK;
+}
+
+namespace {
+
+// ---- Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11) --------------------
+constexpr uint64_t kMul0 = 0xD2E7470EE14C6C93ull;
+constexpr uint64_t kMul1 = 0xCA5A826395121157ull;
+constexpr uint64_t kBump0 = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kBump1 = 0xBB67AE8584CAA73Bull;
+
+enum : uint64_t { kPurposeDelay = 1, kPurposeGraph = 2, kPurposeActivation = 3 };
+
+struct Philox4x64 {
+  uint64_t v[4];
+};
+
+Philox4x64 philox(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3, uint64_t k0, uint64_t k1) {
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += kBump0;
+      k1 += kBump1;
+    }
+    const unsigned __int128 a = (unsigned __int128)kMul0 * c0;
+    const unsigned __int128 b = (unsigned __int128)kMul1 * c2;
+    const uint64_t a_hi = (uint64_t)(a >> 64), a_lo = (uint64_t)a;
+    const uint64_t b_hi = (uint64_t)(b >> 64), b_lo = (uint64_t)b;
+    const uint64_t n0 = b_hi ^ c1 ^ k0, n2 = a_hi ^ c3 ^ k1;
+    c0 = n0;
+    c1 = b_lo;
+    c2 = n2;
+    c3 = a_lo;
+  }
+  return Philox4x64{{c0, c1, c2, c3}};
+}
+
+inline uint64_t draw(uint64_t seed, uint64_t purpose, uint64_t c0, uint64_t c1, uint64_t c2) {
+  return philox(c0, c1, c2, 0, seed, purpose).v[0];
+}
+
+// (0,1): 52 random bits plus one half unit, exact in fp64.
+inline double open_unit(uint64_t w) { return ((double)(w >> 12) + 0.5) * 0x1p-52; }
+
+// [0, k) by multiply-shift.
+inline uint64_t below(uint64_t w, uint64_t k) {
+  return (uint64_t)(((unsigned __int128)w * k) >> 64);
+}
+
+}  // namespace
+}  // namespace nbsgd
+
+using namespace nbsgd;
+
+// ---------------------------------------------------------------- schedule
+extern "C" nbsgd_status nbsgd_sample_mask(uint64_t seed, uint64_t step, int32_t n, int32_t m,
+                                          const nbsgd_delay* d, uint8_t* mask, int32_t* counts,
+                                          double* times, double* timing) {
+  clear_error();
+  if (nbsgd_status st = check_nm(n, m)) return st;
+  if (!d || !mask || !counts) return fail(NBSGD_E_ARG, "d, mask and counts must not be null");
+  if (d->kind < NBSGD_DELAY_CONST || d->kind > NBSGD_DELAY_LOMAX)
+    return fail(NBSGD_E_ARG, "unknown delay kind %d", d->kind);
+  if (d->kind != NBSGD_DELAY_CONST && !(d->param > 0.0))
+    return fail(NBSGD_E_ARG, "delay param %g must be > 0", d->param);
+  if (!(d->base >= 0.0) || !isfinite(d->base)) return fail(NBSGD_E_ARG, "delay base must be >= 0");
+  if (d->slow_learner >= 0 && !(d->slow_factor > 0.0))
+    return fail(NBSGD_E_ARG, "slow_factor %g must be > 0", d->slow_factor);
+
+  double finish[NBSGD_MAX_LEARNERS][NBSGD_MAX_MINIBATCHES];
+  for (int32_t i = 0; i < n; ++i) {
+    const double s = (i == d->slow_learner) ? d->slow_factor : 1.0;
+    double clock = 0.0;
+    for (int32_t j = 0; j < m; ++j) {
+      const double u = open_unit(draw(seed, kPurposeDelay, step, (uint64_t)i, (uint64_t)j));
+      double D = 0.0;
+      if (d->kind == NBSGD_DELAY_EXP)
+        D = -log(u) / d->param;
+      else if (d->kind == NBSGD_DELAY_LOMAX)
+        D = pow(u, -1.0 / d->param) - 1.0;
+      const double t = s * (d->base + D);
+      clock = clock + t;
+      finish[i][j] = clock;
+      if (times) times[i * m + j] = t;
+    }
+  }
+  double T = finish[0][m - 1];
+  for (int32_t i = 1; i < n; ++i) T = std::min(T, finish[i][m - 1]);
+  double t_sync = finish[0][m - 1], t_step = T;
+  for (int32_t i = 0; i < n; ++i) {
+    int32_t c = 0;
+    while (c < m && finish[i][c] <= T) ++c;
+    if (c == 0) c = 1;  // a learner always keeps its first mini-batch
+    counts[i] = c;
+    for (int32_t j = 0; j < m; ++j) mask[i * m + j] = (uint8_t)(j < c);
+    t_sync = std::max(t_sync, finish[i][m - 1]);
+    t_step = std::max(t_step, finish[i][c - 1]);
+  }
+  if (timing) {
+    timing[0] = T;
+    timing[1] = t_sync;
+    timing[2] = t_step;
+  }
+  return NBSGD_OK;
+}
+
+// --------------------------------------------------------- mixing matrices
+extern "C" nbsgd_status nbsgd_w_allreduce(int32_t n, float* W) {
+  clear_error();
+  if (nbsgd_status st = check_nm(n, 1)) return st;
+  if (!W) return fail(NBSGD_E_ARG, "W is null");
+  const float w = (float)(1.0 / (double)n);
+  for (int32_t k = 0; k < n * n; ++k) W[k] = w;
+  return NBSGD_OK;
+}
+
+extern "C" nbsgd_status nbsgd_w_ring(int32_t n, float* W) {
+  clear_error();
+  if (nbsgd_status st = check_nm(n, 1)) return st;
+  if (!W) return fail(NBSGD_E_ARG, "W is null");
+  if (n <= 2) return nbsgd_w_allreduce(n, W);
+  const float third = (float)(1.0 / 3.0);
+  for (int32_t k = 0; k < n * n; ++k) W[k] = 0.0f;
+  for (int32_t i = 0; i < n; ++i) {
+    W[i * n + (i + n - 1) % n] = third;
+    W[i * n + i] = third;
+    W[i * n + (i + 1) % n] = third;
+  }
+  return NBSGD_OK;
+}
+
+struct nbsgd_matcha {
+  uint64_t seed;
+  int32_t n, degree, matchings;
+  double alpha;
+  std::vector<std::pair<int32_t, int32_t>> edges;  // u < v, lexicographic
+  std::vector<int32_t> colour;                     // matching of each edge
+};
+
+namespace {
+
+bool connected(int32_t n, const std::vector<std::pair<int32_t, int32_t>>& edges) {
+  std::vector<std::vector<int32_t>> adj(n);
+  for (auto& e : edges) {
+    adj[e.first].push_back(e.second);
+    adj[e.second].push_back(e.first);
+  }
+  std::vector<char> seen(n, 0);
+  std::vector<int32_t> todo{0};
+  seen[0] = 1;
+  int32_t reached = 1;
+  while (!todo.empty()) {
+    const int32_t u = todo.back();
+    todo.pop_back();
+    for (int32_t v : adj[u])
+      if (!seen[v]) {
+        seen[v] = 1;
+        ++reached;
+        todo.push_back(v);
+      }
+  }
+  return reached == n;
+}
+
+}  // namespace
+
+extern "C" nbsgd_status nbsgd_matcha_create(uint64_t seed, int32_t n, int32_t degree,
+                                            nbsgd_matcha** out) {
+  clear_error();
+  if (!out) return fail(NBSGD_E_ARG, "out is null");
+  *out = nullptr;
+  if (nbsgd_status st = check_nm(n, 1)) return st;
+  if (n < 2 || degree < 1 || degree >= n || (n * degree) % 2)
+    return fail(NBSGD_E_SHAPE, "no simple %d-regular graph on %d nodes", degree, n);
+  const int32_t H = n * degree;
+  std::vector<int32_t> half(H);
+  std::vector<std::pair<int32_t, int32_t>> edges;
+  bool found = false;
+  for (uint64_t attempt = 0; attempt < 100000 && !found; ++attempt) {
+    for (int32_t h = 0; h < H; ++h) half[h] = h;
+    for (int32_t t = H - 1; t >= 1; --t) {
+      const uint64_t r = below(draw(seed, kPurposeGraph, attempt, (uint64_t)t, 0), (uint64_t)t + 1);
+      std::swap(half[t], half[r]);
+    }
+    std::set<std::pair<int32_t, int32_t>> es;
+    bool ok = true;
+    for (int32_t k = 0; k < H && ok; k += 2) {
+      const int32_t u = half[k] / degree, v = half[k + 1] / degree;
+      if (u == v) ok = false;
+      else ok = es.insert({std::min(u, v), std::max(u, v)}).second;
+    }
+    if (!ok) continue;
+    edges.assign(es.begin(), es.end());  // std::set orders lexicographically
+    found = connected(n, edges);
+  }
+  if (!found) return fail(NBSGD_E_SHAPE, "pairing model found no connected simple graph");
+
+  nbsgd_matcha* g = new (std::nothrow) nbsgd_matcha;
+  if (!g) return fail(NBSGD_E_ARG, "out of host memory");
+  g->seed = seed;
+  g->n = n;
+  g->degree = degree;
+  g->alpha = 1.0 / (double)(degree + 1);
+  g->edges = edges;
+  g->colour.assign(edges.size(), 0);
+  std::vector<std::set<int32_t>> used(n);
+  int32_t M = 0;
+  for (size_t k = 0; k < edges.size(); ++k) {
+    const int32_t u = edges[k].first, v = edges[k].second;
+    int32_t c = 0;
+    while (used[u].count(c) || used[v].count(c)) ++c;
+    g->colour[k] = c;
+    used[u].insert(c);
+    used[v].insert(c);
+    M = std::max(M, c + 1);
+  }
+  g->matchings = M;
+  *out = g;
+  return NBSGD_OK;
+}
+
+extern "C" nbsgd_status nbsgd_matcha_w(const nbsgd_matcha* g, uint64_t step, float* W,
+                                       int32_t* n_active) {
+  clear_error();
+  if (!g || !W) return fail(NBSGD_E_ARG, "g and W must not be null");
+  const int32_t n = g->n;
+  std::vector<double> acc((size_t)n * n, 0.0);
+  for (int32_t i = 0; i < n; ++i) acc[(size_t)i * n + i] = 1.0;
+  int32_t active = 0;
+  for (int32_t q = 0; q < g->matchings; ++q) {
+    if ((draw(g->seed, kPurposeActivation, step, (uint64_t)q, 0) >> 63) != 0) continue;
+    ++active;
+    for (size_t k = 0; k < g->edges.size(); ++k) {
+      if (g->colour[k] != q) continue;
+      const int32_t u = g->edges[k].first, v = g->edges[k].second;
+      acc[(size_t)u * n + u] -= g->alpha;
+      acc[(size_t)v * n + v] -= g->alpha;
+      acc[(size_t)u * n + v] += g->alpha;
+      acc[(size_t)v * n + u] += g->alpha;
+    }
+  }
+  for (size_t k = 0; k < acc.size(); ++k) W[k] = (float)acc[k];
+  if (n_active) *n_active = active;
+  return NBSGD_OK;
+}
+
+extern "C" nbsgd_status nbsgd_matcha_matchings(const nbsgd_matcha* g, int32_t* edges_uvq,
+                                               int32_t* E, int32_t* M) {
+  clear_error();
+  if (!g || !E || !M) return fail(NBSGD_E_ARG, "g, E and M must not be null");
+  *E = (int32_t)g->edges.size();
+  *M = g->matchings;
+  if (edges_uvq)
+    for (size_t k = 0; k < g->edges.size(); ++k) {
+      edges_uvq[3 * k + 0] = g->edges[k].first;
+      edges_uvq[3 * k + 1] = g->edges[k].second;
+      edges_uvq[3 * k + 2] = g->colour[k];
+    }
+  return NBSGD_OK;
+}
+
+extern "C" void nbsgd_matcha_destroy(nbsgd_matcha* g) { delete g; }
+
+extern "C" const char* nbsgd_last_error(void) { return g_error.c_str(); }

@@ -1,0 +1,93 @@
+"""Drives the hot path for a workload: device buffers resident in HBM, and per
+iteration the simulated schedule and mixing matrix (host library calls) then
+one fused ``nbsgd_step`` (gfx950 kernel) on the caller's stream.
+
+The host work of iteration k+1 overlaps the kernel of iteration k because the
+step launch is asynchronous and copies its per-step constants into the kernel
+arguments.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+from . import _lib
+from ._lib import DELAY_CONST, DELAY_EXP, DELAY_LOMAX, MIX_THEN_STEP, STEP_THEN_MIX
+
+_DELAY = {"const": DELAY_CONST, "exp": DELAY_EXP, "lomax": DELAY_LOMAX}
+_ORDER = {"mix_then_step": MIX_THEN_STEP, "step_then_mix": STEP_THEN_MIX}
+
+
+class Mixer:
+    """Per-iteration mixing matrix of a workload's kind."""
+
+    def __init__(self, kind: str, n: int, seed: int, degree: int = 3):
+        self.kind = kind
+        self.matcha = None
+        if kind == "uniform":
+            self.fixed = _lib.w_allreduce(n)
+        elif kind == "ring":
+            self.fixed = _lib.w_ring(n)
+        elif kind == "matcha":
+            self.matcha = _lib.Matcha(seed, n, degree)
+        else:
+            raise ValueError(f"unknown mixing kind {kind}")
+
+    def w(self, step: int) -> np.ndarray:
+        if self.matcha is not None:
+            return self.matcha.w(step)[0]
+        return self.fixed
+
+
+class Schedule:
+    """Finished-mini-batch mask of each iteration for a workload's delay model."""
+
+    def __init__(self, wl):
+        d = wl.delay
+        self.args = (wl.n, wl.m, _DELAY[d.kind], d.base, d.param, d.slow_learner, d.slow_factor)
+        self.seed = wl.seed
+
+    def mask(self, step: int):
+        n, m, kind, base, param, slow, factor = self.args
+        return _lib.sample_mask(self.seed, step, n, m, kind, base, param, slow, factor)
+
+
+class StepRunner:
+    """Replicas X, momentum V and gradients G of one workload on a device."""
+
+    def __init__(self, wl, device="cuda:0", P: int | None = None, fill: bool = True):
+        import torch
+
+        from synth import device as synth_device
+        from synth import workloads
+
+        self.wl = wl
+        self.P = wl.P if P is None else P
+        n, m, P = wl.n, wl.m, self.P
+        self.device = torch.device(device)
+        self.X = torch.empty((n, P), dtype=torch.float32, device=self.device)
+        self.V = torch.zeros((n, P), dtype=torch.float32, device=self.device)
+        self.G = torch.empty((n, m, P), dtype=torch.float32, device=self.device)
+        if fill:
+            synth_device.fill_normal(self.X, wl.seed, workloads.STREAM_X, wl.x_std)
+            synth_device.fill_normal(self.G, wl.seed, workloads.STREAM_G, wl.g_std)
+        self.order = _ORDER[wl.order]
+        self.mixer = Mixer(wl.mixing, n, wl.seed, wl.matcha_degree)
+        self.schedule = Schedule(wl)
+
+    def plan(self, step: int):
+        """Host half of iteration ``step``: (mask, counts, timing, W)."""
+        mask, counts, _, timing = self.schedule.mask(step)
+        return mask, counts, timing, self.mixer.w(step)
+
+    def launch(self, mask, W, stream=None):
+        _lib.step(self.X, self.V, self.G, mask, W, self.wl.lr, self.wl.momentum, self.order, stream)
+
+    def run(self, steps: int, first: int = 0, stream=None):
+        """Runs iterations first .. first+steps-1; returns the per-step counts."""
+        out = []
+        for k in range(first, first + steps):
+            mask, counts, _, W = self.plan(k)
+            self.launch(mask, W, stream)
+            out.append(counts)
+        return out

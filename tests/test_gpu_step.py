@@ -1,0 +1,244 @@
+"""GPU parity of the hot path against the CPU oracle, through the C ABI.
+
+Small cases compare every element; full-size workloads run in the launch
+configuration the benchmark times and compare sampled column windows, which
+the oracle regenerates and evolves on its own (columns never interact)."""
+
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2211_00889_amd as nb
+import synth
+from synth import device as synth_device
+from paper_2211_00889_amd import _lib, runner
+from synth import workloads
+from tests._util import (ORACLE_ORDER, TOL, OracleMixer, oracle_delay, oracle_run, rel_err,
+                         window_inputs)
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _say(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def _birkhoff_w(rng, n, terms=3):
+    """Random doubly stochastic matrix: convex combination of permutations
+    (not symmetric, so a transposed W would be caught)."""
+    lam = rng.dirichlet(np.ones(terms))
+    W = np.zeros((n, n))
+    for a in lam:
+        W[np.arange(n), rng.permutation(n)] += a
+    return W.astype(np.float32)
+
+
+def _inputs(rng, n, m, P):
+    X = rng.standard_normal((n, P)).astype(np.float32)
+    V = (0.1 * rng.standard_normal((n, P))).astype(np.float32)
+    G = (0.03 * rng.standard_normal((n, m, P))).astype(np.float32)
+    return X, V, G
+
+
+def _random_mask(rng, n, m, prefix=True):
+    if prefix:
+        c = rng.integers(1, m + 1, size=n)
+        return (np.arange(m)[None, :] < c[:, None]).astype(np.uint8)
+    mask = (rng.random((n, m)) < 0.5).astype(np.uint8)
+    mask[np.arange(n), rng.integers(0, m, size=n)] = 1
+    return mask
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 4, 5, 63, 64, 65, 255, 256, 257, 258, 1030, 4099, 20000])
+def test_fill_matches_host_generator(P):
+    _say(f"fill P={P}")
+    t = torch.empty(3 * P, dtype=torch.float32, device=DEV)
+    synth_device.fill_normal(t, 4, 9, 0.5)
+    assert np.array_equal(t.cpu().numpy(), synth.normal_f32(4, 9, np.arange(3 * P), 0.5))
+    synth_device.fill_uniform(t, 4, 9, 0.25)
+    assert np.array_equal(t.cpu().numpy(), synth.uniform_f32(4, 9, np.arange(3 * P), 0.25))
+
+
+CASES = [  # n, m, P: vector widths 4/2/1, one and several tiles, ragged tails
+    (1, 1, 1), (1, 3, 7), (2, 2, 6), (3, 5, 257), (4, 4, 1030), (5, 7, 4099), (8, 8, 256),
+    (8, 8, 20002), (16, 4, 4096), (16, 64, 515), (7, 64, 130), (16, 1, 1000),
+]
+
+
+@pytest.mark.parametrize("order", [nb.MIX_THEN_STEP, nb.STEP_THEN_MIX])
+@pytest.mark.parametrize("n,m,P", CASES)
+def test_step_matches_oracle(n, m, P, order):
+    rng = np.random.default_rng(n * 1000 + m * 10 + P + order)
+    X, V, G = _inputs(rng, n, m, P)
+    for trial, (mask, W) in enumerate([
+            (_random_mask(rng, n, m), _birkhoff_w(rng, n)),
+            (_random_mask(rng, n, m, prefix=False), np.full((n, n), np.float32(1.0 / n))),
+            (np.ones((n, m), np.uint8), oracle.mixing.w_ring(n).astype(np.float32))]):
+        _say(f"step n={n} m={m} P={P} order={order} trial={trial}")
+        Xd, Vd, Gd = _dev(X), _dev(V), _dev(G)
+        nb.step(Xd, Vd, Gd, mask, W, 0.1, 0.9, order)
+        torch.cuda.synchronize()
+        Xo, Vo = oracle.step.step(X, V, G, mask, W.astype(np.float64), float(np.float32(0.1)),
+                                  float(np.float32(0.9)), order)
+        assert rel_err(Vd.cpu().numpy(), Vo) <= TOL
+        assert rel_err(Xd.cpu().numpy(), Xo) <= TOL
+        assert np.array_equal(Gd.cpu().numpy(), G)  # G is read-only
+
+
+@pytest.mark.parametrize("n,m,P", [(4, 4, 1030), (8, 16, 4098), (16, 4, 999), (3, 2, 5)])
+def test_unfused_stages_and_compositions(n, m, P):
+    rng = np.random.default_rng(P)
+    X, V, G = _inputs(rng, n, m, P)
+    mask = _random_mask(rng, n, m, prefix=False)
+    counts = mask.sum(axis=1).astype(np.int32)
+    W = _birkhoff_w(rng, n)
+    lr, mu = float(np.float32(0.2)), float(np.float32(0.8))
+    _say(f"accumulate n={n} m={m} P={P}")
+    Gd, Gbar = _dev(G), torch.empty(n, P, dtype=torch.float32, device=DEV)
+    nb.accumulate(Gd, mask, Gbar)
+    torch.cuda.synchronize()
+    gbar_o = oracle.step.accumulate(G, mask)
+    assert rel_err(Gbar.cpu().numpy(), gbar_o) <= TOL
+    _say(f"mix n={n} P={P}")
+    Xd, Yd = _dev(X), torch.empty(n, P, dtype=torch.float32, device=DEV)
+    nb.mix(Xd, W, Yd)
+    torch.cuda.synchronize()
+    assert rel_err(Yd.cpu().numpy(), oracle.step.mix(W.astype(np.float64), X)) <= TOL
+    _say(f"update n={n} P={P}")
+    Xd, Vd = _dev(X), _dev(V)
+    nb.update(Xd, Vd, _dev(gbar_o.astype(np.float32)), counts, m, 0.2, 0.8)
+    torch.cuda.synchronize()
+    eta = oracle.step.learning_rates(counts, m, lr)
+    Vo = oracle.step.momentum(V, gbar_o.astype(np.float32).astype(np.float64), mu)
+    assert rel_err(Vd.cpu().numpy(), Vo) <= TOL
+    assert rel_err(Xd.cpu().numpy(), X - eta[:, None] * Vo) <= TOL
+    for order in (nb.MIX_THEN_STEP, nb.STEP_THEN_MIX):
+        _say(f"composition order={order} n={n} P={P}")
+        Xd, Vd, Gd = _dev(X), _dev(V), _dev(G)
+        Gbar = torch.empty(n, P, dtype=torch.float32, device=DEV)
+        nb.accumulate(Gd, mask, Gbar)
+        if order == nb.MIX_THEN_STEP:
+            Yd = torch.empty_like(Xd)
+            nb.mix(Xd, W, Yd)
+            nb.update(Yd, Vd, Gbar, counts, m, 0.2, 0.8)
+            Xd = Yd
+        else:
+            nb.update(Xd, Vd, Gbar, counts, m, 0.2, 0.8)
+            nb.mix(Xd, W, Xd)  # in place
+        torch.cuda.synchronize()
+        Xo, Vo = oracle.step.step(X, V, G, mask, W.astype(np.float64), lr, mu, order)
+        assert rel_err(Vd.cpu().numpy(), Vo) <= TOL
+        assert rel_err(Xd.cpu().numpy(), Xo) <= TOL
+
+
+def test_mix_in_place_and_uniform_rows_identical():
+    n, P = 8, 70001
+    rng = np.random.default_rng(1)
+    X = rng.standard_normal((n, P)).astype(np.float32)
+    _say("mix in place, uniform")
+    Xd = _dev(X)
+    nb.mix(Xd, nb.w_allreduce(n), Xd)
+    out = Xd.cpu().numpy()
+    assert all(np.array_equal(out[0], out[i]) for i in range(n))
+    assert rel_err(out, oracle.step.mix(oracle.mixing.w_uniform(n), X)) <= TOL
+    _say("mix in place, ring")
+    Xd = _dev(X)
+    nb.mix(Xd, nb.w_ring(n), Xd)
+    assert rel_err(Xd.cpu().numpy(), oracle.step.mix(oracle.mixing.w_ring(n), X)) <= TOL
+
+
+def test_full_mask_allreduce_replicas_identical_and_deterministic():
+    n, m, P = 8, 4, 33333
+    rng = np.random.default_rng(2)
+    X, V, G = _inputs(rng, n, m, P)
+    outs = []
+    for rep in range(2):
+        _say(f"allreduce identical rep={rep}")
+        Xd, Vd, Gd = _dev(X), _dev(V), _dev(G)
+        for _ in range(3):
+            nb.step(Xd, Vd, Gd, np.ones((n, m), np.uint8), nb.w_allreduce(n), 0.1, 0.9,
+                    nb.STEP_THEN_MIX)
+        out = Xd.cpu().numpy()
+        assert all(np.array_equal(out[0], out[i]) for i in range(n))
+        outs.append((out, Vd.cpu().numpy()))
+    assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])
+
+
+def test_tiny_workload_every_step():
+    """The 4-learner workload end to end, both orders, compared after every step."""
+    wl = workloads.TINY
+    for order in (workloads.STEP_THEN_MIX, workloads.MIX_THEN_STEP):
+        w = dataclasses.replace(wl, order=order)
+        _say(f"tiny workload order={order}")
+        r = runner.StepRunner(w, DEV)
+        X0, G = window_inputs(w, np.arange(w.P))
+        assert np.array_equal(r.X.cpu().numpy(), X0) and np.array_equal(r.G.cpu().numpy(), G)
+        Xo, Vo = X0.astype(np.float64), np.zeros((w.n, w.P))
+        mixer = OracleMixer(w)
+        d = oracle_delay(w)
+        for k in range(w.steps):
+            mask, counts, timing, W = r.plan(k)
+            s = oracle.schedule.sample_schedule(w.seed, k, w.n, w.m, d)
+            assert np.array_equal(mask, s["mask"]) and np.array_equal(counts, s["counts"])
+            assert np.array_equal(W, mixer.w(k).astype(np.float32))
+            r.launch(mask, W)
+            Xo, Vo = oracle.step.step(Xo, Vo, G, s["mask"], mixer.w(k), float(np.float32(w.lr)),
+                                      float(np.float32(w.momentum)), ORACLE_ORDER[order])
+            torch.cuda.synchronize()
+            assert rel_err(r.V.cpu().numpy(), Vo) <= TOL, k
+            assert rel_err(r.X.cpu().numpy(), Xo) <= TOL, k
+
+
+def _windows(P, seed, k=8, width=4096, edge=65536):
+    rng = np.random.default_rng(seed)
+    cols = [np.arange(0, min(edge, P)), np.arange(max(0, P - edge), P)]
+    for s in rng.integers(0, P - width, size=k):
+        cols.append(np.arange(s, s + width))
+    return np.unique(np.concatenate(cols))
+
+
+@pytest.mark.parametrize("name", ["resnet18", "resnet50", "vgg16"])
+def test_full_size_workload_sampled_columns(name):
+    """Full-size workload, every iteration, bench launch configuration;
+    compared on sampled column windows (first, last and random)."""
+    wl = workloads.get(name)
+    _say(f"full size {wl.name}: n={wl.n} m={wl.m} P={wl.P} steps={wl.steps}")
+    r = runner.StepRunner(wl, DEV)
+    counts = r.run(wl.steps)
+    torch.cuda.synchronize()
+    cols = _windows(wl.P, 11)
+    idx = torch.from_numpy(cols).to(DEV)
+    Xg = r.X.index_select(1, idx).cpu().numpy()
+    Vg = r.V.index_select(1, idx).cpu().numpy()
+    del r
+    torch.cuda.empty_cache()
+    X0, G = window_inputs(wl, cols)
+    Xo, Vo, masks = oracle_run(wl, X0, G, wl.steps)
+    for k in range(wl.steps):
+        assert np.array_equal(counts[k], masks[k].sum(axis=1)), k
+    assert rel_err(Vg, Vo) <= TOL
+    assert rel_err(Xg, Xo) <= TOL
+
+
+def test_gpu_argument_errors():
+    n, m, P = 4, 4, 1000
+    X = torch.zeros(n * P + 1, dtype=torch.float32, device=DEV)
+    V = torch.zeros(n, P, dtype=torch.float32, device=DEV)
+    G = torch.zeros(n, m, P, dtype=torch.float32, device=DEV)
+    _say("misaligned X")
+    with pytest.raises(nb.NbsgdError) as e:
+        nb.step(X[1:].view(n, P), V, G, np.ones((n, m)), nb.w_ring(n), 0.1, 0.9, 0)
+    assert e.value.status == _lib.E_ALIGN
+    with pytest.raises(nb.NbsgdError) as e:
+        nb.step(V, V, G, np.ones((n, m)), nb.w_ring(n), 0.1, 0.9, 0)
+    assert e.value.status == _lib.E_ARG
+    torch.cuda.synchronize()
