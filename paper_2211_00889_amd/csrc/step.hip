@@ -9,14 +9,22 @@
 // place.  Rows are streamed as VEC-wide vectors (VEC = 4 when P % 4 == 0, else
 // 2 or 1), so each wave moves 64 * VEC * 4 contiguous bytes per row per load.
 //
-// Fused step, one workgroup = 4 waves x (64 lanes * U vectors) columns:
-//   phase 1: wave w takes learners p = w, w+4, ...; for its columns it reads
-//            X[p], V[p] and only the finished rows of G[p], forms the new
-//            momentum (stored at once) and the value to be mixed, z_p = x_p
+// Fused step, one workgroup = 8 waves x 64 lanes, one VEC-vector column per
+// lane, all n learners:
+//   phase 1: the finished gradient rows of the tile (sum_i c_i of them, in
+//            learner-major order) are split into 8 equal contiguous segments,
+//            one per wave, so a straggler-skewed mask (one learner with all m
+//            rows, another with one) still gives every wave the same number
+//            of loads.  A wave sums each learner's rows within its segment and
+//            writes the partial sum to an LDS slot; wave w also loads X and V
+//            of learners w and w + 8 into registers.
+//   phase 2: wave w adds the slots of its learners in slot order (a fixed
+//            order, so results are bitwise reproducible), forms the momentum
+//            (stored at once) and the value to be mixed, z_p = x_p
 //            (mix-then-step) or x_p - eta_p v_p (step-then-mix), into LDS;
-//   phase 2: after one barrier, wave w forms row i = w, w+4, ... of the mix
-//            from LDS (CSR of the nonzero W entries, or one sum scaled by 1/n
-//            for uniform W) and writes X[i].
+//   phase 3: wave w forms row i = w, w + 8 of the mix from LDS (CSR of the
+//            nonzero W entries, or one sum scaled by 1/n for uniform W) and
+//            writes X[i].
 // HBM traffic per step is the finished rows of G once, X and V read once and
 // written once: 4 * P * (sum_i c_i + 4 n) bytes.
 #include <hip/hip_runtime.h>
@@ -37,6 +45,13 @@ constexpr int kMaxN = NBSGD_MAX_LEARNERS;
 constexpr int kMaxM = NBSGD_MAX_MINIBATCHES;
 constexpr int kSlots = (kMaxN + kWaves - 1) / kWaves;  // learners per wave
 
+// fused step kernel shape
+constexpr int kStepWaves = 8;
+constexpr int kStepBlock = kWave * kStepWaves;
+constexpr int kStepSlots = (kMaxN + kStepWaves - 1) / kStepWaves;
+constexpr int kMaxRows = kMaxN * kMaxM;           // finished rows of one step
+constexpr int kMaxRuns = kMaxN + kStepWaves - 1;  // partial-sum slots
+
 template <int VEC>
 struct Vec;
 template <>
@@ -52,6 +67,25 @@ struct Vec<1> {
   typedef float type;
 };
 
+// Kernel arguments are only ever read as naturally aligned 32-bit words:
+// sub-word arrays are packed into uint32_t and unpacked with shifts.  (A
+// dynamically indexed uint8_t array next to 32-bit fields let the compiler
+// form a scalar-load base address that was not 4-byte aligned; the scalar
+// memory unit ignores the low two address bits, so neighbouring fields were
+// read one element early.)
+__host__ __device__ __forceinline__ uint32_t byte_of(const uint32_t* words, int i) {
+  return (words[i >> 2] >> (8 * (i & 3))) & 0xffu;
+}
+__host__ __device__ __forceinline__ uint32_t half_of(const uint32_t* words, int i) {
+  return (words[i >> 1] >> (16 * (i & 1))) & 0xffffu;
+}
+__host__ __device__ __forceinline__ void set_byte(uint32_t* words, int i, uint32_t v) {
+  words[i >> 2] |= (v & 0xffu) << (8 * (i & 3));
+}
+__host__ __device__ __forceinline__ void set_half(uint32_t* words, int i, uint32_t v) {
+  words[i >> 1] |= (v & 0xffffu) << (16 * (i & 1));
+}
+
 // Per-learner constants of one step, passed by value in the kernel arguments.
 struct Learners {
   float eta[kMaxN];           // lr * c_i / m
@@ -63,7 +97,7 @@ struct Learners {
 };
 
 __device__ __forceinline__ int row_of(const Learners& L, int p, int r) {
-  return (int)((L.rows[p][r >> 2] >> (8 * (r & 3))) & 0xffu);
+  return (int)byte_of(L.rows[p], r);
 }
 
 // Mixing matrix as CSR over its nonzero entries, or the uniform flag.
@@ -71,8 +105,24 @@ struct Mixing {
   int32_t uniform;   // all entries equal: out = (sum_p z_p) * w_all
   float w_all;
   int32_t start[kMaxN + 1];
-  uint8_t col[kMaxN * kMaxN];
+  uint32_t col[kMaxN * kMaxN / 4];  // column of each entry, 8 bits each
   float w[kMaxN * kMaxN];
+};
+
+// Per-step plan of the fused kernel, passed by value in the kernel arguments.
+// Entries are the finished (learner, mini-batch) pairs in learner-major
+// order; wave w sums entries [seg[w], seg[w+1]).  A run is a maximal stretch
+// of one learner's entries inside one wave's segment; runs are numbered in
+// entry order and each owns one LDS slot.
+struct StepPlan {
+  float eta[kMaxN];                    // lr * c_i / m
+  float inv_c[kMaxN];                  // 1 / c_i
+  int32_t prefix[kMaxN + 2];           // first entry of each learner; [n] = [n+1] = total
+  int32_t seg[kStepWaves + 1];         // first entry of each wave's segment
+  int32_t seg_p[kStepWaves];           // learner of a segment's first entry
+  int32_t seg_slot[kStepWaves];        // slot of a segment's first run
+  int32_t lslot[kMaxN + 1];            // slots of learner p: [lslot[p], lslot[p+1])
+  uint32_t row[(kMaxRows + 16) / 2];   // G row (p * m + j) of each entry, 16 bits each
 };
 
 template <typename T>
@@ -84,7 +134,12 @@ __device__ __forceinline__ void st_stream(T* p, T v) {
   __builtin_nontemporal_store(v, p);
 }
 
-// Sum of the finished rows of learner p at vector column v.
+// Number of finished-row loads a thread keeps in flight before summing them.
+constexpr int kChunk = 16;
+
+// Sum of the finished rows of learner p at vector column v.  Rows are loaded
+// kChunk at a time (the tail chunk predicated on the uniform count) so each
+// wave has kChunk independent 64 x VEC x 4-byte loads in flight.
 template <int VEC>
 __device__ __forceinline__ typename Vec<VEC>::type finished_sum(const typename Vec<VEC>::type* G,
                                                                 const Learners& L, int p, int m,
@@ -93,22 +148,16 @@ __device__ __forceinline__ typename Vec<VEC>::type finished_sum(const typename V
   const vf* g = G + (int64_t)p * m * pv + v;
   const int c = L.count[p];
   vf acc = (vf)(0.0f);
-  int r = 0;
-  for (; r + 4 <= c; r += 4) {
-    const uint32_t w = L.rows[p][r >> 2];
-    const vf a0 = ld_stream(g + (int64_t)(w & 0xffu) * pv);
-    const vf a1 = ld_stream(g + (int64_t)((w >> 8) & 0xffu) * pv);
-    const vf a2 = ld_stream(g + (int64_t)((w >> 16) & 0xffu) * pv);
-    const vf a3 = ld_stream(g + (int64_t)(w >> 24) * pv);
-    acc += (a0 + a1) + (a2 + a3);
-  }
-  const int rem = c - r;  // 0..3 rows left, loaded together
-  if (rem > 0) {
-    const vf a0 = ld_stream(g + (int64_t)row_of(L, p, r) * pv);
-    vf a1 = (vf)(0.0f), a2 = (vf)(0.0f);
-    if (rem > 1) a1 = ld_stream(g + (int64_t)row_of(L, p, r + 1) * pv);
-    if (rem > 2) a2 = ld_stream(g + (int64_t)row_of(L, p, r + 2) * pv);
-    acc += (a0 + a1) + a2;
+  for (int r = 0; r < c; r += kChunk) {
+    vf a[kChunk];
+#pragma unroll
+    for (int k = 0; k < kChunk; ++k)
+      a[k] = (r + k < c) ? ld_stream(g + (int64_t)row_of(L, p, r + k) * pv) : (vf)(0.0f);
+#pragma unroll
+    for (int w = 1; w < kChunk; w *= 2)
+#pragma unroll
+      for (int k = 0; k < kChunk; k += 2 * w) a[k] += a[k + w];
+    acc += a[0];
   }
   return acc;
 }
@@ -120,7 +169,8 @@ __device__ __forceinline__ typename Vec<VEC>::type mix_row(const typename Vec<VE
                                                            int t) {
   using vf = typename Vec<VEC>::type;
   vf acc = (vf)(0.0f);
-  for (int e = W.start[i]; e < W.start[i + 1]; ++e) acc += W.w[e] * zs[W.col[e] * ncols + t];
+  for (int e = W.start[i]; e < W.start[i + 1]; ++e)
+    acc += W.w[e] * zs[(int)byte_of(W.col, e) * ncols + t];
   return acc;
 }
 
@@ -133,68 +183,97 @@ __device__ __forceinline__ typename Vec<VEC>::type mix_all(const typename Vec<VE
   return acc;
 }
 
-template <int VEC, int U, int ORDER>
-__global__ void __launch_bounds__(kBlock)
+template <int VEC, int ORDER>
+__global__ void __launch_bounds__(kStepBlock)
     k_step(float* __restrict__ Xf, float* __restrict__ Vf, const float* __restrict__ Gf,
-           int64_t pv, int n, int m, float mu, Learners L, Mixing W) {
+           int64_t pv, int n, float mu, StepPlan S, Mixing W) {
   using vf = typename Vec<VEC>::type;
   extern __shared__ char smem[];
-  vf* zs = reinterpret_cast<vf*>(smem);  // [n][U * 64]
-  constexpr int ncols = U * kWave;
+  vf* zs = reinterpret_cast<vf*>(smem);        // [n][64]: values to be mixed
+  vf* part = zs + n * kWave;                   // [runs][64]: partial row sums
   vf* X = reinterpret_cast<vf*>(Xf);
   vf* V = reinterpret_cast<vf*>(Vf);
   const vf* G = reinterpret_cast<const vf*>(Gf);
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int64_t col0 = (int64_t)blockIdx.x * ncols;
+  const int64_t v = (int64_t)blockIdx.x * kWave + lane;
+  const bool live = v < pv;
 
-  vf keep[kSlots][U];  // eta_i * v_i for mix-then-step
+  // phase 1: own learners' X and V, and this wave's share of the G rows
+  vf xo[kStepSlots], vo[kStepSlots];
 #pragma unroll
-  for (int s = 0; s < kSlots; ++s) {
-    const int p = wave + kWaves * s;
-    if (p < n) {
+  for (int s = 0; s < kStepSlots; ++s) {
+    const int p = wave + kStepWaves * s;
+    xo[s] = (vf)(0.0f);
+    vo[s] = (vf)(0.0f);
+    if (p < n && live) {
+      xo[s] = ld_stream(X + (int64_t)p * pv + v);
+      vo[s] = ld_stream(V + (int64_t)p * pv + v);
+    }
+  }
+  const int e_end = S.seg[wave + 1];
+  int p = S.seg_p[wave];
+  int slot = S.seg_slot[wave];
+  int next = S.prefix[p + 1];  // entry where learner p's rows end
+  vf acc = (vf)(0.0f);
+  bool open = false;
+  for (int e = S.seg[wave]; e < e_end; e += kChunk) {
+    vf a[kChunk];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int t = lane + kWave * u;
-        const int64_t v = col0 + t;
-        if (v < pv) {
-          const int64_t off = (int64_t)p * pv + v;
-          const vf x = ld_stream(X + off);
-          const vf vo = ld_stream(V + off);
-          const vf g = finished_sum<VEC>(G, L, p, m, pv, v);
-          const vf vn = mu * vo + g * L.inv_c[p];
-          st_stream(V + off, vn);
-          if (ORDER == NBSGD_MIX_THEN_STEP) {
-            zs[p * ncols + t] = x;
-            keep[s][u] = L.eta[p] * vn;
-          } else {
-            zs[p * ncols + t] = x - L.eta[p] * vn;
-          }
+    for (int k = 0; k < kChunk; ++k) {
+      const int64_t row = (e + k < e_end) ? (int64_t)half_of(S.row, e + k) : 0;  // uniform
+      a[k] = (e + k < e_end && live) ? ld_stream(G + row * pv + v) : (vf)(0.0f);
+    }
+#pragma unroll
+    for (int k = 0; k < kChunk; ++k) {
+      if (e + k < e_end) {
+        acc += a[k];
+        open = true;
+        if (e + k + 1 == next) {  // learner p's rows end here: close the run
+          part[slot * kWave + lane] = acc;
+          acc = (vf)(0.0f);
+          open = false;
+          ++slot;
+          ++p;
+          next = S.prefix[p + 1];
         }
       }
     }
   }
+  if (open) part[slot * kWave + lane] = acc;
   __syncthreads();
-  vf total[U];
-  if (W.uniform) {
+
+  // phase 2: combine partial sums in slot order, momentum, value to be mixed
+  vf keep[kStepSlots];  // eta_i * v_i for mix-then-step
 #pragma unroll
-    for (int u = 0; u < U; ++u) total[u] = mix_all<VEC>(zs, ncols, n, lane + kWave * u) * W.w_all;
-  }
-#pragma unroll
-  for (int s = 0; s < kSlots; ++s) {
-    const int i = wave + kWaves * s;
-    if (i < n) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int t = lane + kWave * u;
-        const int64_t v = col0 + t;
-        if (v < pv) {
-          vf x = W.uniform ? total[u] : mix_row<VEC>(zs, ncols, W, i, t);
-          if (ORDER == NBSGD_MIX_THEN_STEP) x -= keep[s][u];
-          st_stream(X + (int64_t)i * pv + v, x);
-        }
+  for (int s = 0; s < kStepSlots; ++s) {
+    const int q = wave + kStepWaves * s;
+    if (q < n) {
+      vf g = (vf)(0.0f);
+      for (int r = S.lslot[q]; r < S.lslot[q + 1]; ++r) g += part[r * kWave + lane];
+      const vf vn = mu * vo[s] + g * S.inv_c[q];
+      if (live) st_stream(V + (int64_t)q * pv + v, vn);
+      if (ORDER == NBSGD_MIX_THEN_STEP) {
+        zs[q * kWave + lane] = xo[s];
+        keep[s] = S.eta[q] * vn;
+      } else {
+        zs[q * kWave + lane] = xo[s] - S.eta[q] * vn;
       }
+    }
+  }
+  __syncthreads();
+
+  // phase 3: mix and write the new replicas
+  vf total = (vf)(0.0f);
+  if (W.uniform) total = mix_all<VEC>(zs, kWave, n, lane) * W.w_all;
+#pragma unroll
+  for (int s = 0; s < kStepSlots; ++s) {
+    const int i = wave + kStepWaves * s;
+    if (i < n && live) {
+      vf x = W.uniform ? total : mix_row<VEC>(zs, kWave, W, i, lane);
+      if (ORDER == NBSGD_MIX_THEN_STEP) x -= keep[s];
+      st_stream(X + (int64_t)i * pv + v, x);
     }
   }
 }
@@ -295,7 +374,7 @@ nbsgd_status mixing_from_w(const float* Wh, int32_t n, Mixing* W) {
     W->start[i] = e;
     for (int32_t p = 0; p < n; ++p)
       if (Wh[i * n + p] != 0.0f) {
-        W->col[e] = (uint8_t)p;
+        set_byte(W->col, e, (uint32_t)p);
         W->w[e] = Wh[i * n + p];
         ++e;
       }
@@ -316,16 +395,52 @@ nbsgd_status check_rows(const void* p, const char* name) {
   return NBSGD_OK;
 }
 
-constexpr int kStepU = 1;
+static_assert(sizeof(StepPlan) + sizeof(Mixing) + 64 <= 4096, "kernel arguments exceed 4 KiB");
+
+nbsgd_status plan_from_mask(const uint8_t* mask, int32_t n, int32_t m, float lr, StepPlan* S,
+                            int* runs) {
+  if (!mask) return fail(NBSGD_E_ARG, "mask is null");
+  memset(S, 0, sizeof *S);
+  int32_t e = 0;
+  int learner_of[kMaxRows];
+  for (int32_t i = 0; i < n; ++i) {
+    S->prefix[i] = e;
+    for (int32_t j = 0; j < m; ++j)
+      if (mask[i * m + j]) {
+        learner_of[e] = i;
+        set_half(S->row, e++, (uint32_t)(i * m + j));
+      }
+    const int32_t c = e - S->prefix[i];
+    if (c == 0) return fail(NBSGD_E_MASK, "learner %d finished no mini-batch", i);
+    S->inv_c[i] = (float)(1.0 / (double)c);
+    S->eta[i] = (float)((double)lr * (double)c / (double)m);
+  }
+  S->prefix[n] = S->prefix[n + 1] = e;
+  int slot = 0, last_learner = -1;
+  for (int w = 0; w <= kStepWaves; ++w) S->seg[w] = (int32_t)((int64_t)w * e / kStepWaves);
+  for (int w = 0; w < kStepWaves; ++w) {
+    S->seg_slot[w] = slot;
+    if (S->seg[w] == S->seg[w + 1]) continue;
+    S->seg_p[w] = learner_of[S->seg[w]];
+    for (int32_t k = S->seg[w]; k < S->seg[w + 1]; ++k) {
+      const bool starts_run = k == S->seg[w] || learner_of[k] != learner_of[k - 1];
+      if (!starts_run) continue;
+      while (last_learner < learner_of[k]) S->lslot[++last_learner] = slot;
+      ++slot;
+    }
+  }
+  while (last_learner < n) S->lslot[++last_learner] = slot;
+  *runs = slot;
+  return NBSGD_OK;
+}
 
 template <int VEC, int ORDER>
-void launch_step(float* X, float* V, const float* G, int64_t pv, int n, int m, float mu,
-                 const Learners& L, const Mixing& W, hipStream_t s) {
-  constexpr int ncols = kStepU * kWave;
-  const int64_t blocks = (pv + ncols - 1) / ncols;
-  const size_t lds = (size_t)n * ncols * VEC * sizeof(float);
-  hipLaunchKernelGGL((k_step<VEC, kStepU, ORDER>), dim3((unsigned)blocks), dim3(kBlock), lds, s, X,
-                     V, G, pv, n, m, mu, L, W);
+void launch_step(float* X, float* V, const float* G, int64_t pv, int n, float mu,
+                 const StepPlan& S, int runs, const Mixing& W, hipStream_t s) {
+  const int64_t blocks = (pv + kWave - 1) / kWave;
+  const size_t lds = (size_t)(n + runs) * kWave * VEC * sizeof(float);
+  hipLaunchKernelGGL((k_step<VEC, ORDER>), dim3((unsigned)blocks), dim3(kStepBlock), lds, s, X,
+                     V, G, pv, n, mu, S, W);
 }
 
 }  // namespace
@@ -338,8 +453,9 @@ extern "C" nbsgd_status nbsgd_step(float* X, float* V, const float* G, const uin
   if (P < 0) return fail(NBSGD_E_SHAPE, "P=%lld is negative", (long long)P);
   if (order != NBSGD_MIX_THEN_STEP && order != NBSGD_STEP_THEN_MIX)
     return fail(NBSGD_E_ARG, "unknown order %d", order);
-  Learners L;
-  if (nbsgd_status st = learners_from_mask(mask, n, m, lr, &L)) return st;
+  StepPlan S;
+  int runs = 0;
+  if (nbsgd_status st = plan_from_mask(mask, n, m, lr, &S, &runs)) return st;
   Mixing W;
   if (nbsgd_status st = mixing_from_w(Wh, n, &W)) return st;
   if (P == 0) return NBSGD_OK;
@@ -352,17 +468,17 @@ extern "C" nbsgd_status nbsgd_step(float* X, float* V, const float* G, const uin
     return fail(NBSGD_E_ARG, "G overlaps X or V");
   const int vec = vec_width(P);
   const int64_t pv = P / vec;
-  if ((pv + kStepU * kWave - 1) / (kStepU * kWave) > 0x7fffffff)
+  if ((pv + kWave - 1) / kWave > 0x7fffffff)
     return fail(NBSGD_E_UNSUPPORTED, "P=%lld needs too many workgroups", (long long)P);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (order == NBSGD_MIX_THEN_STEP) {
-    if (vec == 4) launch_step<4, NBSGD_MIX_THEN_STEP>(X, V, G, pv, n, m, momentum, L, W, s);
-    else if (vec == 2) launch_step<2, NBSGD_MIX_THEN_STEP>(X, V, G, pv, n, m, momentum, L, W, s);
-    else launch_step<1, NBSGD_MIX_THEN_STEP>(X, V, G, pv, n, m, momentum, L, W, s);
+    if (vec == 4) launch_step<4, NBSGD_MIX_THEN_STEP>(X, V, G, pv, n, momentum, S, runs, W, s);
+    else if (vec == 2) launch_step<2, NBSGD_MIX_THEN_STEP>(X, V, G, pv, n, momentum, S, runs, W, s);
+    else launch_step<1, NBSGD_MIX_THEN_STEP>(X, V, G, pv, n, momentum, S, runs, W, s);
   } else {
-    if (vec == 4) launch_step<4, NBSGD_STEP_THEN_MIX>(X, V, G, pv, n, m, momentum, L, W, s);
-    else if (vec == 2) launch_step<2, NBSGD_STEP_THEN_MIX>(X, V, G, pv, n, m, momentum, L, W, s);
-    else launch_step<1, NBSGD_STEP_THEN_MIX>(X, V, G, pv, n, m, momentum, L, W, s);
+    if (vec == 4) launch_step<4, NBSGD_STEP_THEN_MIX>(X, V, G, pv, n, momentum, S, runs, W, s);
+    else if (vec == 2) launch_step<2, NBSGD_STEP_THEN_MIX>(X, V, G, pv, n, momentum, S, runs, W, s);
+    else launch_step<1, NBSGD_STEP_THEN_MIX>(X, V, G, pv, n, momentum, S, runs, W, s);
   }
   return check_launch("nbsgd_step");
 }
