@@ -35,6 +35,24 @@ METRIC = "learner-param updates/sec and achieved HBM GB/s (% peak) for fused nbs
 UNIT = "learner-param updates/s"
 
 
+def measured_traffic(wl):
+    """HBM bytes per launch of the fused kernel from the committed rocprofv3
+    PMC summary (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter
+    reads for a plain 1 GiB copy), or None when there is no summary for this
+    workload or the kernel source changed since the counters were taken."""
+    import glob
+    import hashlib
+
+    src = os.path.join(ROOT, "paper_2211_00889_amd", "csrc", "step.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    for path in glob.glob(os.path.join(ROOT, "profiles", "k_step_traffic_*.json")):
+        with open(path) as f:
+            rec = json.load(f)
+        if rec.get("workload") == wl.name and rec.get("kernel_source_sha256") == sha:
+            return rec
+    return None
+
+
 def cpu_baseline(wl, budget_s: float = 15.0, cols: int = 1 << 19):
     """The oracle on columns [0, cols) of the workload, one thread, about
     ``budget_s`` seconds; returns learner-param updates per second."""
@@ -74,6 +92,9 @@ def main():
     ap.add_argument("--workload", default="resnet18")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="after the timed steps, run one plain 1 GiB device copy (torch's copy "
+                         "kernel) so hardware byte counters can be scaled against known bytes")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the simulated learners are replicas in one "
@@ -139,8 +160,20 @@ def main():
                      "kernel_ms_median": float(np.median(kern_ms)),
                      "alg_bytes_per_launch_mean": float(alg_bytes.mean())},
     }
+    rec = measured_traffic(wl)
+    if rec is not None:
+        out["roofline"]["traffic"] = rec["traffic_bytes_per_launch"]
+        out["roofline"]["traffic_over_alg"] = rec["traffic_over_alg"]
+        out["roofline"]["traffic_dispatches"] = f"{rec['dispatches']} launches, steps {rec['steps']}"
     del r
     torch.cuda.empty_cache()
+    if args.calibration_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)
