@@ -192,6 +192,79 @@ nbsgd_status nbsgd_matcha_matchings(const nbsgd_matcha *g, int32_t *edges_uvq, i
                                     int32_t *M);
 void nbsgd_matcha_destroy(nbsgd_matcha *g);
 
+/* -------------------------------------------------- end-to-end MLP workload
+ * Learners train a two-layer perceptron, d_in -> hidden (ReLU) -> classes with
+ * softmax cross-entropy, on a data set split into n equal shards (Alg. 1/2
+ * initialisation; Eq. 1 with the per-sample cross-entropy as l).
+ * Flat parameter layout of one replica row: W1[d_in][hidden] row-major,
+ * b1[hidden], W2[hidden][classes], b2[classes].
+ * Supported shapes: batch == 32, d_in a multiple of 128, hidden a multiple of 64,
+ * hidden <= 512, 2 <= classes <= 16 (NBSGD_E_UNSUPPORTED otherwise).        */
+typedef struct {
+  int32_t d_in, hidden, classes, batch;
+} nbsgd_mlp_shape;
+
+/* Parameters per replica (d_in*hidden + hidden + hidden*classes + classes). */
+nbsgd_status nbsgd_mlp_param_count(const nbsgd_mlp_shape *s, int64_t *P);
+
+/* Device workspace, in bytes, for calls that process up to `rows` sample rows:
+ * n*m*batch for nbsgd_mlp_grad, `count` for nbsgd_mlp_loss.  The caller
+ * allocates it once (16-byte aligned) and may reuse it for every call on the
+ * same stream; calls that overlap on different streams need their own.      */
+nbsgd_status nbsgd_mlp_workspace_bytes(const nbsgd_mlp_shape *s, int64_t rows, size_t *bytes);
+
+/* Local shuffling (Alg. 1/2 initialisation and "shuffle local subset after
+ * each epoch"; Sec. 3.2 shuffling bullet).  Learner i owns samples
+ * [shard*i, shard*(i+1)).  Local epoch e permutes its shard by Fisher-Yates
+ * from the top (position t swaps with floor(w*(t+1)/2^64), w = Philox4x64-10
+ * word 0 at counter (e, i, t, 0) under key (seed, 4)); iteration `step` is
+ * window step mod (shard / (m*b)) of epoch step div (shard / (m*b)), and
+ * mini-batch j is the j-th run of b samples of that window.  Windows are
+ * consumed whether or not their mini-batches finish.
+ * idx: host int32 [n][m][b], global sample indices (caller-owned).
+ * Errors: NBSGD_E_ARG (null idx), NBSGD_E_SHAPE (shard < m*b, b < 1),
+ *         NBSGD_E_UNSUPPORTED.                                              */
+nbsgd_status nbsgd_minibatch_indices(uint64_t seed, uint64_t step, int32_t n, int32_t m, int32_t b,
+                                     int32_t shard, int32_t *idx);
+
+/* Per-mini-batch gradients (Alg. 2 "compute the local stochastic gradient",
+ * Sec. 3.2 "compute gradients") of every finished mini-batch, each at its
+ * learner's replica:
+ *   G[i][j][:] = gradient of the mean cross-entropy of the 32 samples
+ *                idx[i][j][:] at parameters X[i], for mask[i*m+j] != 0;
+ *   losses[i*m+j] = that mean loss.
+ * Unfinished rows of G and entries of losses are left untouched.  Every GEMM
+ * input (the samples, W1, bf16(ReLU(Z1)), W2, dZ2, dZ1) is rounded to bf16
+ * (nearest even) and multiplied on the matrix cores with fp32 accumulation;
+ * bias, ReLU, softmax and cross-entropy are fp32.
+ * X      device fp32 [n][P] (P from nbsgd_mlp_param_count)
+ * data   device fp32 [n_samples][d_in]; labels device int32 [n_samples] in
+ *        [0, classes) (values outside are clamped into range)
+ * idx    host int32 [n*m*batch], every value in [0, n_samples) (NBSGD_E_ARG);
+ *        read before the call returns (copied through kernel arguments)
+ * mask   host uint8 [n*m]
+ * G      device fp32 [n][m][P]; losses device fp32 [n*m]
+ * workspace  device, >= nbsgd_mlp_workspace_bytes(s, n*m*batch)
+ * Errors: NBSGD_E_ARG, NBSGD_E_SHAPE, NBSGD_E_ALIGN, NBSGD_E_UNSUPPORTED,
+ *         NBSGD_E_HIP.                                                      */
+nbsgd_status nbsgd_mlp_grad(const float *X, int32_t n, int32_t m, const nbsgd_mlp_shape *s,
+                            const float *data, const int32_t *labels, int64_t n_samples,
+                            const int32_t *idx, const uint8_t *mask, float *G, float *losses,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+/* Mean cross-entropy of one parameter vector on `count` samples, in batches
+ * of 32: losses[k] = mean loss of samples idx[32k .. 32k+31] (same precision
+ * as nbsgd_mlp_grad's forward pass).  Used to evaluate the average of the
+ * replicas, the method's output (Alg. 1/2 output line).
+ * params device fp32 [P]; idx host int32 [count], count a multiple of 32 and
+ * at most 16384; losses device fp32 [count / 32].
+ * workspace  device, >= nbsgd_mlp_workspace_bytes(s, count)
+ * Errors: as nbsgd_mlp_grad.                                                */
+nbsgd_status nbsgd_mlp_loss(const float *params, const nbsgd_mlp_shape *s, const float *data,
+                            const int32_t *labels, int64_t n_samples, const int32_t *idx,
+                            int32_t count, float *losses, void *workspace, size_t workspace_bytes,
+                            void *stream);
+
 /* ---------------------------------------------------------------- errors
  * Text of the last failed check or HIP error on the calling thread ("" if
  * none).  The pointer stays valid until the next nbsgd call on the thread. */

@@ -28,4 +28,4 @@ Parity pins for each function live in ``tests/test_oracle_*.py``; functions
 with no pin say "parity unpinned" in their docstring.
 """
 
-from . import mixing, philox, schedule, step  # noqa: F401
+from . import mixing, mlp, philox, schedule, step  # noqa: F401

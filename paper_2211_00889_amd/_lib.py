@@ -24,13 +24,20 @@ MAX_LEARNERS, MAX_MINIBATCHES = 16, 64
 
 EXPORTS = ("nbsgd_sample_mask", "nbsgd_accumulate", "nbsgd_mix", "nbsgd_update", "nbsgd_step",
            "nbsgd_w_allreduce", "nbsgd_w_ring", "nbsgd_matcha_create", "nbsgd_matcha_w",
-           "nbsgd_matcha_matchings", "nbsgd_matcha_destroy", "nbsgd_last_error")
+           "nbsgd_matcha_matchings", "nbsgd_matcha_destroy", "nbsgd_mlp_param_count",
+           "nbsgd_mlp_workspace_bytes", "nbsgd_minibatch_indices", "nbsgd_mlp_grad",
+           "nbsgd_mlp_loss", "nbsgd_last_error")
 
 
 class NbsgdError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"nbsgd status {status}: {message}")
         self.status = status
+
+
+class MlpShape(ctypes.Structure):
+    _fields_ = [("d_in", ctypes.c_int32), ("hidden", ctypes.c_int32), ("classes", ctypes.c_int32),
+                ("batch", ctypes.c_int32)]
 
 
 class Delay(ctypes.Structure):
@@ -64,6 +71,14 @@ def load():
         "nbsgd_matcha_create": [_u64, _i32, _i32, ctypes.POINTER(_c_void_p)],
         "nbsgd_matcha_w": [_c_void_p, _u64, _c_void_p, _c_void_p],
         "nbsgd_matcha_matchings": [_c_void_p, _c_void_p, _c_void_p, _c_void_p],
+        "nbsgd_mlp_param_count": [ctypes.POINTER(MlpShape), ctypes.POINTER(_i64)],
+        "nbsgd_mlp_workspace_bytes": [ctypes.POINTER(MlpShape), _i64, ctypes.POINTER(ctypes.c_size_t)],
+        "nbsgd_minibatch_indices": [_u64, _u64, _i32, _i32, _i32, _i32, _c_void_p],
+        "nbsgd_mlp_grad": [_c_void_p, _i32, _i32, ctypes.POINTER(MlpShape), _c_void_p, _c_void_p, _i64,
+                           _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, ctypes.c_size_t,
+                           _c_void_p],
+        "nbsgd_mlp_loss": [_c_void_p, ctypes.POINTER(MlpShape), _c_void_p, _c_void_p, _i64, _c_void_p,
+                           _i32, _c_void_p, _c_void_p, ctypes.c_size_t, _c_void_p],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -213,3 +228,65 @@ def step(X, V, G, mask, W, lr: float, momentum: float, order: int, stream=None):
     W = _w32(W, n)
     _check(load().nbsgd_step(_dev(X, "X"), _dev(V, "V"), _dev(G, "G"), _host_ptr(mask),
                              _host_ptr(W), n, m, P, lr, momentum, order, _stream(X, stream)))
+
+
+# ------------------------------------------------------------ MLP workload
+def _shape(d_in, hidden, classes, batch=32):
+    return MlpShape(d_in, hidden, classes, batch)
+
+
+def mlp_param_count(d_in: int, hidden: int, classes: int, batch: int = 32) -> int:
+    P = _i64(0)
+    _check(load().nbsgd_mlp_param_count(ctypes.byref(_shape(d_in, hidden, classes, batch)),
+                                        ctypes.byref(P)))
+    return P.value
+
+
+def mlp_workspace_bytes(d_in: int, hidden: int, classes: int, rows: int, batch: int = 32) -> int:
+    b = ctypes.c_size_t(0)
+    _check(load().nbsgd_mlp_workspace_bytes(ctypes.byref(_shape(d_in, hidden, classes, batch)), rows,
+                                            ctypes.byref(b)))
+    return b.value
+
+
+def minibatch_indices(seed: int, step: int, n: int, m: int, b: int, shard: int) -> np.ndarray:
+    idx = np.zeros((max(n, 0), max(m, 0), max(b, 0)), np.int32)
+    _check(load().nbsgd_minibatch_indices(seed, step, n, m, b, shard, _host_ptr(idx)))
+    return idx
+
+
+def _i32_dev(t, name):
+    import torch
+
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.int32 or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous int32 CUDA tensor")
+    return _c_void_p(t.data_ptr())
+
+
+def _ws(t):
+    import torch
+
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
+        raise TypeError("workspace must be a contiguous CUDA tensor")
+    return _c_void_p(t.data_ptr()), t.numel() * t.element_size()
+
+
+def mlp_grad(X, m: int, dims, data, labels, idx, mask, G, losses, workspace, stream=None):
+    """dims = (d_in, hidden, classes); idx host int32 [n, m, 32]; mask host [n, m]."""
+    n = X.shape[0]
+    idx = np.ascontiguousarray(np.asarray(idx), dtype=np.int32)
+    mask = _u8(mask, (n, m))
+    ws, ws_bytes = _ws(workspace)
+    _check(load().nbsgd_mlp_grad(_dev(X, "X"), n, m, ctypes.byref(_shape(*dims)), _dev(data, "data"),
+                                 _i32_dev(labels, "labels"), data.shape[0], _host_ptr(idx),
+                                 _host_ptr(mask), _dev(G, "G"), _dev(losses, "losses"), ws, ws_bytes,
+                                 _stream(X, stream)))
+
+
+def mlp_loss(params, dims, data, labels, idx, losses, workspace, stream=None):
+    """Mean loss of ``params`` on the samples ``idx`` (host int32), per 32."""
+    idx = np.ascontiguousarray(np.asarray(idx), dtype=np.int32).reshape(-1)
+    ws, ws_bytes = _ws(workspace)
+    _check(load().nbsgd_mlp_loss(_dev(params, "params"), ctypes.byref(_shape(*dims)), _dev(data, "data"),
+                                 _i32_dev(labels, "labels"), data.shape[0], _host_ptr(idx), idx.size,
+                                 _dev(losses, "losses"), ws, ws_bytes, _stream(params, stream)))

@@ -51,7 +51,11 @@ def build(verbose: bool = False) -> None:
     step_o = os.path.join(OBJ, "step.o")
     _run([HIPCC, *HIP_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "step.hip"),
           "-o", step_o], verbose)
-    _atomic_link([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", host_o, step_o], LIB, verbose)
+    mlp_o = os.path.join(OBJ, "mlp.o")
+    _run([HIPCC, *HIP_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "mlp.hip"),
+          "-o", mlp_o], verbose)
+    _atomic_link([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", host_o, step_o, mlp_o], LIB,
+                 verbose)
     _atomic_link([HIPCC, *HIP_FLAGS, "-shared", os.path.join(ROOT, "synth", "fill.hip")],
                  SYNTH_LIB, verbose)
 

@@ -70,7 +70,7 @@ constexpr uint64_t kMul1 = 0xCA5A826395121157ull;
 constexpr uint64_t kBump0 = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kBump1 = 0xBB67AE8584CAA73Bull;
 
-enum : uint64_t { kPurposeDelay = 1, kPurposeGraph = 2, kPurposeActivation = 3 };
+enum : uint64_t { kPurposeDelay = 1, kPurposeGraph = 2, kPurposeActivation = 3, kPurposeShuffle = 4 };
 
 struct Philox4x64 {
   uint64_t v[4];
@@ -322,3 +322,30 @@ extern "C" nbsgd_status nbsgd_matcha_matchings(const nbsgd_matcha* g, int32_t* e
 extern "C" void nbsgd_matcha_destroy(nbsgd_matcha* g) { delete g; }
 
 extern "C" const char* nbsgd_last_error(void) { return g_error.c_str(); }
+
+// ------------------------------------------------------------ local shuffle
+extern "C" nbsgd_status nbsgd_minibatch_indices(uint64_t seed, uint64_t step, int32_t n, int32_t m,
+                                                int32_t b, int32_t shard, int32_t* idx) {
+  clear_error();
+  if (nbsgd_status st = check_nm(n, m)) return st;
+  if (!idx) return fail(NBSGD_E_ARG, "idx is null");
+  if (b < 1 || shard < (int64_t)m * b)
+    return fail(NBSGD_E_SHAPE, "shard=%d must hold at least m*b=%lld samples", shard,
+                (long long)m * b);
+  const int64_t per_epoch = shard / ((int64_t)m * b);
+  const uint64_t epoch = step / (uint64_t)per_epoch;
+  const int64_t window = (int64_t)(step % (uint64_t)per_epoch);
+  std::vector<int32_t> perm(shard);
+  for (int32_t i = 0; i < n; ++i) {
+    for (int32_t t = 0; t < shard; ++t) perm[t] = t;
+    for (int32_t t = shard - 1; t >= 1; --t) {
+      const uint64_t r = below(draw(seed, kPurposeShuffle, epoch, (uint64_t)i, (uint64_t)t),
+                               (uint64_t)t + 1);
+      std::swap(perm[t], perm[r]);
+    }
+    const int64_t base = window * m * b;
+    for (int64_t k = 0; k < (int64_t)m * b; ++k)
+      idx[(int64_t)i * m * b + k] = (int32_t)((int64_t)shard * i + perm[base + k]);
+  }
+  return NBSGD_OK;
+}

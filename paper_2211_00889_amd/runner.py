@@ -91,3 +91,61 @@ class StepRunner:
             self.launch(mask, W, stream)
             out.append(counts)
         return out
+
+
+class MlpRunner:
+    """The end-to-end workload on a device: synthetic data and labels, n
+    identical initial replicas, and per iteration the schedule, the shuffled
+    mini-batch indices, the per-mini-batch gradients (bf16 MFMA) and the fused
+    step."""
+
+    def __init__(self, wl, device="cuda:0", data=None, labels=None, x0=None):
+        import torch
+
+        from synth import mlp_data
+
+        self.wl = wl
+        self.dims = (wl.d_in, wl.hidden, wl.classes)
+        self.P = _lib.mlp_param_count(*self.dims)
+        dev = self.device = torch.device(device)
+        if data is None:
+            data = mlp_data.inputs(wl.seed, wl.n_samples, wl.d_in)
+        if labels is None:
+            labels = mlp_data.teacher_labels(wl.seed, data, wl.hidden, wl.classes)
+        if x0 is None:
+            x0 = mlp_data.student_init(wl.seed, wl.d_in, wl.hidden, wl.classes)
+        self.data = torch.from_numpy(np.ascontiguousarray(data, dtype=np.float32)).to(dev)
+        self.labels = torch.from_numpy(np.ascontiguousarray(labels, dtype=np.int32)).to(dev)
+        self.X = torch.from_numpy(np.ascontiguousarray(x0, dtype=np.float32)).to(dev).repeat(wl.n, 1)
+        self.V = torch.zeros_like(self.X)
+        self.G = torch.zeros((wl.n, wl.m, self.P), dtype=torch.float32, device=dev)
+        self.losses = torch.zeros(wl.n * wl.m, dtype=torch.float32, device=dev)
+        self.eval_idx = wl.eval_indices()
+        self.eval_losses = torch.zeros(len(self.eval_idx) // wl.batch, dtype=torch.float32, device=dev)
+        rows = max(wl.n * wl.m * wl.batch, len(self.eval_idx))
+        ws = _lib.mlp_workspace_bytes(*self.dims, rows)
+        self.workspace = torch.empty((ws + 15) // 16 * 4, dtype=torch.float32, device=dev)
+        self.mean = torch.empty_like(self.X)
+        self.mixer = Mixer(wl.mixing, wl.n, wl.seed)
+        self.schedule = Schedule(wl)
+        self.order = _ORDER[wl.order]
+        self.w_mean = _lib.w_allreduce(wl.n)
+
+    def step(self, k: int, stream=None):
+        """Iteration k; returns (mask, counts).  The finished mini-batches'
+        losses are left in ``self.losses`` (index i*m + j)."""
+        wl = self.wl
+        mask, counts, _, _ = self.schedule.mask(k)
+        idx = _lib.minibatch_indices(wl.seed, k, wl.n, wl.m, wl.batch, wl.shard)
+        _lib.mlp_grad(self.X, wl.m, self.dims, self.data, self.labels, idx, mask, self.G, self.losses,
+                      self.workspace, stream)
+        _lib.step(self.X, self.V, self.G, mask, self.mixer.w(k), wl.lr, wl.momentum, self.order, stream)
+        return mask, counts
+
+    def evaluate(self, stream=None):
+        """Loss of the average replica (the method's output) on the fixed
+        evaluation samples, per batch of 32 (device tensor)."""
+        _lib.mix(self.X, self.w_mean, self.mean, stream)
+        _lib.mlp_loss(self.mean[0], self.dims, self.data, self.labels, self.eval_idx, self.eval_losses,
+                      self.workspace, stream)
+        return self.eval_losses

@@ -75,3 +75,45 @@ ALIASES = {"tiny": TINY.name, "resnet18": RESNET18_RING.name, "resnet50": RESNET
 
 def get(name: str) -> Workload:
     return WORKLOADS[ALIASES.get(name, name)]
+
+
+@dataclass(frozen=True)
+class MlpWorkload:
+    """End-to-end workload: n learners train a d_in -> hidden (ReLU) ->
+    classes softmax MLP by Non-blocking D-PSGD on a ring."""
+    name: str
+    n: int = 8
+    m: int = 8
+    batch: int = 32
+    d_in: int = 3072
+    hidden: int = 512
+    classes: int = 10
+    n_samples: int = 50_000
+    mixing: str = "ring"
+    order: str = MIX_THEN_STEP
+    delay: DelaySpec = DelaySpec("exp", 1.0, 1.0)
+    lr: float = 0.05
+    momentum: float = 0.9
+    steps: int = 200
+    seed: int = 0
+    eval_every: int = 10
+    eval_samples: int = 4096
+    eval_stride: int = 12      # evaluation subset: samples 0, 12, 24, ...
+
+    @property
+    def P(self) -> int:
+        return self.d_in * self.hidden + self.hidden + self.hidden * self.classes + self.classes
+
+    @property
+    def shard(self) -> int:
+        return self.n_samples // self.n
+
+    def eval_indices(self):
+        import numpy as np
+
+        return (np.arange(self.eval_samples, dtype=np.int64) * self.eval_stride).astype(np.int32)
+
+
+MLP = MlpWorkload("mlp_n8_m8_b32_3072x512x10_ring")
+MLP_TINY = MlpWorkload("mlp_tiny_n4_m4_b32_128x64x10_ring", n=4, m=4, d_in=128, hidden=64,
+                       n_samples=4 * 640, steps=12, eval_every=4, eval_samples=256, eval_stride=10)

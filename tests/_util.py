@@ -81,4 +81,21 @@ def oracle_run(wl, X0, G, steps, first=0):
     return X, V, masks
 
 
-__all__ = ["TOL", "rel_err", "window_inputs", "oracle_run", "OracleMixer", "oracle_delay", "gen"]
+
+
+def mlp_blocks(d_in, hidden, classes):
+    """(name, start, stop) of the W1, b1, W2, b2 blocks of a flat MLP vector."""
+    b1 = d_in * hidden
+    w2 = b1 + hidden
+    b2 = w2 + hidden * classes
+    return [("W1", 0, b1), ("b1", b1, w2), ("W2", w2, b2), ("b2", b2, b2 + classes)]
+
+
+def rel_err_blocks(got, want, blocks) -> float:
+    """Largest per-block rel_err along the last axis: each parameter block is
+    measured against its own rms, so blocks of very different scale (1.57M
+    first-layer weights beside 10 output biases) do not hide or inflate each
+    other."""
+    got = np.asarray(got)
+    want = np.asarray(want)
+    return max(rel_err(got[..., a:b], want[..., a:b]) for _, a, b in blocks)

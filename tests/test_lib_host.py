@@ -152,3 +152,48 @@ def test_device_call_argument_errors_launch_nothing():
                          ctypes.c_void_p(X + 64), None) == _lib.E_ARG   # partial overlap
     assert lib.nbsgd_accumulate(ctypes.c_void_p(G), bad.ctypes.data_as(ctypes.c_void_p), n, m, P,
                                 ctypes.c_void_p(X), None) == _lib.E_MASK
+
+
+@pytest.mark.parametrize("n,m,b,shard", [(8, 8, 32, 6250), (4, 4, 32, 640), (3, 2, 5, 23), (1, 1, 1, 1)])
+def test_minibatch_indices_bitwise(n, m, b, shard):
+    sh = oracle.mlp.Shuffler(7, shard, m, b)
+    per = shard // (m * b)
+    for step in sorted({0, 1, per - 1, per, 2 * per + 1, 25}):
+        idx = nb._lib.minibatch_indices(7, step, n, m, b, shard)
+        for i in range(n):
+            assert np.array_equal(idx[i], sh.indices(step, i)), (step, i)
+
+
+def test_minibatch_indices_errors():
+    with pytest.raises(nb.NbsgdError) as e:
+        nb._lib.minibatch_indices(0, 0, 2, 4, 32, 100)  # shard < m * b
+    assert e.value.status == _lib.E_SHAPE
+
+
+def test_mlp_shape_checks():
+    assert nb._lib.mlp_param_count(3072, 512, 10) == 1_578_506
+    for bad in ((3000, 512, 10), (3072, 520, 10), (3072, 1024, 10), (3072, 512, 17), (3072, 512, 1)):
+        with pytest.raises(nb.NbsgdError) as e:
+            nb._lib.mlp_param_count(*bad)
+        assert e.value.status == _lib.E_UNSUPPORTED
+    with pytest.raises(nb.NbsgdError) as e:
+        nb._lib.mlp_param_count(3072, 512, 10, batch=16)
+    assert e.value.status == _lib.E_UNSUPPORTED
+
+
+def test_mlp_grad_rejects_bad_indices_before_launch():
+    # fake device pointers: the host rejects the sample list before any launch
+    lib = _lib.load()
+    shape = _lib.MlpShape(128, 64, 10, 32)
+    n, m = 2, 2
+    idx = np.zeros(n * m * 32, np.int32)
+    idx[5] = 100  # n_samples = 100 -> out of range
+    mask = np.ones(n * m, np.uint8)
+    ws = _lib.mlp_workspace_bytes(128, 64, 10, n * m * 32)
+    p = ctypes.c_void_p(0x100000)
+    rc = lib.nbsgd_mlp_grad(p, n, m, ctypes.byref(shape), p, p, 100, idx.ctypes.data_as(ctypes.c_void_p),
+                            mask.ctypes.data_as(ctypes.c_void_p), p, p, p, ws, None)
+    assert rc == _lib.E_ARG and b"position 5" in lib.nbsgd_last_error()
+    rc = lib.nbsgd_mlp_grad(p, n, m, ctypes.byref(shape), p, p, 100, idx.ctypes.data_as(ctypes.c_void_p),
+                            mask.ctypes.data_as(ctypes.c_void_p), p, p, p, ws - 1, None)
+    assert rc == _lib.E_ARG and b"workspace" in lib.nbsgd_last_error()
