@@ -103,7 +103,7 @@ def bench_mlp(args):
     finished = 0
     t0 = time.perf_counter()
     for k in range(args.warmup, args.warmup + args.steps):
-        mask, counts = r.step(k)
+        mask, counts, _ = r.step(k)
         finished += int(counts.sum())
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0

@@ -64,20 +64,33 @@ typedef enum {
  * (Eq. 4-5 ring all-reduce, Eq. 6 D-PSGD, Alg. 3). */
 typedef enum { NBSGD_MIX_THEN_STEP = 0, NBSGD_STEP_THEN_MIX = 1 } nbsgd_order;
 
-/* Per-mini-batch time model: t = s_i * (base + D), s_i = slow_factor for
- * learner slow_learner (-1: none) and 1 otherwise.
+/* Per-mini-batch time model: t = s_i * (base + D) with the learner's
+ * slow-down s_i:
+ *   slow_learner >= 0: s_i = slow_factor for that learner, 1 for the others;
+ *   slow_learner == NBSGD_SLOW_NONE (-1): s_i = 1;
+ *   slow_learner == NBSGD_SLOW_RANDOM (-2): the paper's heterogeneity model
+ *     (Sec. 6.1: the slowed nodes and the rate of slow-down change every
+ *     iteration, the slowest node taking up to twice as long): at each
+ *     iteration every learner is slowed with probability slow_prob, by a
+ *     factor 1 + (slow_factor - 1) * u, u uniform in (0, 1) (words 0 and 1
+ *     of Philox4x64-10 at counter (step, i, 0, 0) under key (seed, 5): slowed
+ *     iff u0 < slow_prob, factor from u1, both mapped as below).
  *   CONST: D = 0
  *   EXP:   D ~ Exp(rate = param), mean 1/param (App. A, Remark 1)
  *   LOMAX: D = Pareto type II with shape param, so base 1 + D is Pareto with
  *          scale 1 (heavy-tailed stragglers)                                  */
 typedef enum { NBSGD_DELAY_CONST = 0, NBSGD_DELAY_EXP = 1, NBSGD_DELAY_LOMAX = 2 } nbsgd_delay_kind;
 
+#define NBSGD_SLOW_NONE (-1)
+#define NBSGD_SLOW_RANDOM (-2)
+
 typedef struct {
   int32_t kind;        /* nbsgd_delay_kind */
   double base;         /* >= 0 */
   double param;        /* EXP: rate > 0; LOMAX: shape > 0; CONST: ignored */
   int32_t slow_learner;
-  double slow_factor;  /* > 0 */
+  double slow_factor;  /* > 0; >= 1 for NBSGD_SLOW_RANDOM */
+  double slow_prob;    /* NBSGD_SLOW_RANDOM only: in [0, 1] */
 } nbsgd_delay;
 
 /* ---------------------------------------------------------------- schedule
@@ -94,7 +107,8 @@ typedef struct {
  *   times  double[n*m] (nullable): t[i][j]
  *   timing double[3]   (nullable): {T, T_sync = max_i C[i][m-1] (the blocking
  *          iteration time), T_step = max(T, max_i C[i][c_i-1])}
- * Errors: NBSGD_E_ARG (null mask/counts/d, bad kind or non-positive param),
+ * Errors: NBSGD_E_ARG (null mask/counts/d, bad kind or non-positive param,
+ *         slow_learner below -2 or at least n, a slow-down outside its range),
  *         NBSGD_E_SHAPE, NBSGD_E_UNSUPPORTED.                                  */
 nbsgd_status nbsgd_sample_mask(uint64_t seed, uint64_t step, int32_t n, int32_t m,
                                const nbsgd_delay *d, uint8_t *mask, int32_t *counts,
@@ -147,7 +161,10 @@ nbsgd_status nbsgd_update(float *X, float *V, const float *Gbar, const int32_t *
  *   MIX_THEN_STEP: X[i] = sum_p W[i*n+p] X[p] - eta_i V[i]
  *   STEP_THEN_MIX: X[i] = sum_p W[i*n+p] (X[p] - eta_p V[p])
  * Equal, up to fp32 rounding, to accumulate + mix + update (MIX_THEN_STEP) or
- * accumulate + update + mix (STEP_THEN_MIX).
+ * accumulate + update + mix (STEP_THEN_MIX).  Non-blocking synchronous
+ * centralized SGD (Alg. 3, with the 1/n of Eq. 2) is STEP_THEN_MIX with the
+ * uniform W on replicas that all hold the server model: every row of X then
+ * becomes x_ps - (1/n) sum_i eta_i V[i].
  * X, V  device fp32 [n][P], updated in place; G device fp32 [n][m][P], must
  *       not overlap X or V; X and V must not overlap.
  * mask, W as above; order is an nbsgd_order.

@@ -150,7 +150,7 @@ class Shuffler:
 
 
 # ------------------------------------------------------------------ training
-def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None):
+def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None, blocking: bool = False):
     """Non-blocking D-PSGD on the MLP (Alg. 2): every iteration draws the
     schedule, computes the gradient of each finished mini-batch at the
     learner's own replica, then mixes and steps with the ring W.
@@ -168,7 +168,7 @@ def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None):
     n, m, P = wl.n, wl.m, s.n_params
     kinds = {"const": schedule.DELAY_CONST, "exp": schedule.DELAY_EXP, "lomax": schedule.DELAY_LOMAX}
     d = schedule.Delay(kinds[wl.delay.kind], wl.delay.base, wl.delay.param, wl.delay.slow_learner,
-                       wl.delay.slow_factor)
+                       wl.delay.slow_factor, wl.delay.slow_prob)
     W = mixing.w_ring(n).astype(np.float32).astype(np.float64)
     order = step_mod.MIX_THEN_STEP if wl.order == "mix_then_step" else step_mod.STEP_THEN_MIX
     lr, mu = float(np.float32(wl.lr)), float(np.float32(wl.momentum))
@@ -176,7 +176,7 @@ def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None):
     X = np.tile(np.asarray(x0, dtype=np.float64), (n, 1))
     V = np.zeros_like(X)
     ev_idx = wl.eval_indices()
-    out = dict(step_loss=[], counts=[], eval_step=[], eval_loss=[])
+    out = dict(step_loss=[], counts=[], eval_step=[], eval_loss=[], seconds=[])
 
     def evaluate(k):
         xbar = X.mean(axis=0)
@@ -190,6 +190,12 @@ def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None):
         if k % wl.eval_every == 0:
             evaluate(k)
         sch = schedule.sample_schedule(wl.seed, k, n, m, d)
+        if blocking:
+            sch["mask"] = np.ones((n, m), dtype=np.uint8)
+            sch["counts"] = np.full(n, m, dtype=np.int32)
+            out["seconds"].append(sch["t_sync"])
+        else:
+            out["seconds"].append(sch["t_step"])
         learner_losses = []
         for i in range(n):
             idx = shuf.indices(k, i)

@@ -13,6 +13,7 @@ Conventions used by the simulated schedule (key = (seed, purpose)):
 * purpose 2: MATCHA base graph, counter (attempt, position, 0, 0)
 * purpose 3: MATCHA matching activation, counter (step, matching, 0, 0)
 * purpose 4: local shuffles of the MLP workload, counter (epoch, learner, position, 0)
+* purpose 5: per-iteration random slow-down, counter (step, learner, 0, 0)
 
 Pins: the all-zero block equals the published Random123 known answer, and
 blocks agree with NumPy's independent ``numpy.random.Philox`` (tests).
@@ -30,6 +31,7 @@ PURPOSE_DELAY = 1
 PURPOSE_GRAPH = 2
 PURPOSE_ACTIVATION = 3
 PURPOSE_SHUFFLE = 4
+PURPOSE_SLOWDOWN = 5
 
 
 def block(counter, key, rounds: int = 10):

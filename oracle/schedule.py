@@ -19,7 +19,14 @@ Delay models (rate convention for Exp, mean 1/rate, as in Remark 1 of App. A):
 * LOMAX:  D = u**(-1/shape) - 1   (so base 1 plus D is Pareto with scale 1)
 
 t[i, j] = s_i * (base + D) where s_i is ``slow_factor`` for the one slowed
-learner and 1 otherwise.  u comes from Philox word 0 at counter
+learner and 1 otherwise, or, with ``slow_learner = SLOW_RANDOM``, the paper's
+heterogeneity model (Sec. 6.1: which nodes are slowed and by how much changes
+every iteration, the slowest taking up to twice as long): every iteration
+each learner is slowed with probability ``slow_prob`` by a factor uniform
+between 1 and ``slow_factor`` (Philox words 0 and 1 at counter (step, i, 0, 0)
+under key (seed, 5)).
+
+The delay variate u of mini-batch j comes from Philox word 0 at counter
 (step, i, j, 0) under key (seed, 1).  Scalar ``math.log`` / ``math.pow`` are
 used on purpose (the platform libm, one value at a time).
 """
@@ -36,6 +43,8 @@ from . import philox
 DELAY_CONST = 0
 DELAY_EXP = 1
 DELAY_LOMAX = 2
+SLOW_NONE = -1
+SLOW_RANDOM = -2
 
 
 @dataclass(frozen=True)
@@ -43,8 +52,9 @@ class Delay:
     kind: int = DELAY_EXP
     base: float = 1.0
     param: float = 1.0          # EXP: rate; LOMAX: shape
-    slow_learner: int = -1      # -1: nobody is slowed
+    slow_learner: int = -1      # -1: nobody is slowed; -2: random per iteration
     slow_factor: float = 1.0
+    slow_prob: float = 0.0      # random slow-down only
 
 
 def minibatch_time(seed: int, step: int, i: int, j: int, d: Delay) -> float:
@@ -58,8 +68,17 @@ def minibatch_time(seed: int, step: int, i: int, j: int, d: Delay) -> float:
         extra = math.pow(u, -1.0 / d.param) - 1.0
     else:
         raise ValueError(f"unknown delay kind {d.kind}")
-    scale = d.slow_factor if i == d.slow_learner else 1.0
-    return scale * (d.base + extra)
+    return slowdown(seed, step, i, d) * (d.base + extra)
+
+
+def slowdown(seed: int, step: int, i: int, d: Delay) -> float:
+    """s_i of learner i in iteration ``step``."""
+    if d.slow_learner == SLOW_RANDOM:
+        w0, w1, _, _ = philox.block((step, i, 0, 0), (seed, philox.PURPOSE_SLOWDOWN))
+        if philox.u01(w0) < d.slow_prob:
+            return 1.0 + (d.slow_factor - 1.0) * philox.u01(w1)
+        return 1.0
+    return d.slow_factor if i == d.slow_learner else 1.0
 
 
 def sample_schedule(seed: int, step: int, n: int, m: int, d: Delay) -> dict:

@@ -88,3 +88,24 @@ def step(X, V, G, mask, W, lr: float, mu: float, order: int):
     else:
         raise ValueError(f"unknown order {order}")
     return X_new, V_new
+
+
+def parameter_server_step(x_ps, V, G, mask, lr: float, mu: float):
+    """Non-blocking synchronous centralized SGD (Alg. 3): every learner
+    computes its accumulated gradient at the server's model, the server
+    subtracts the learners' lr * c_i / m scaled steps, averaged over the n
+    learners (Alg. 3 omits the 1/n of Eq. 2; it is restored here), and every
+    learner takes the new server model.  With momentum, each learner keeps its
+    own buffer v_i <- mu v_i + g_i and contributes eta_i v_i.
+
+    x_ps: [P]; V: [n, P]; G: [n, m, P].  Returns (x_ps', V') in fp64."""
+    G = np.asarray(G)
+    n, m, _ = G.shape
+    counts = finished_counts(mask)
+    g = accumulate(G, mask)
+    eta = learning_rates(counts, m, lr)
+    V_new = momentum(V, g, mu)
+    x = np.asarray(x_ps, dtype=np.float64).copy()
+    for i in range(n):
+        x = x - (eta[i] / n) * V_new[i]
+    return x, V_new

@@ -21,6 +21,7 @@ OK, E_ARG, E_SHAPE, E_ALIGN, E_MASK, E_W, E_HIP, E_UNSUPPORTED = range(8)
 MIX_THEN_STEP, STEP_THEN_MIX = 0, 1
 DELAY_CONST, DELAY_EXP, DELAY_LOMAX = 0, 1, 2
 MAX_LEARNERS, MAX_MINIBATCHES = 16, 64
+SLOW_NONE, SLOW_RANDOM = -1, -2
 
 EXPORTS = ("nbsgd_sample_mask", "nbsgd_accumulate", "nbsgd_mix", "nbsgd_update", "nbsgd_step",
            "nbsgd_w_allreduce", "nbsgd_w_ring", "nbsgd_matcha_create", "nbsgd_matcha_w",
@@ -42,7 +43,8 @@ class MlpShape(ctypes.Structure):
 
 class Delay(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("base", ctypes.c_double), ("param", ctypes.c_double),
-                ("slow_learner", ctypes.c_int32), ("slow_factor", ctypes.c_double)]
+                ("slow_learner", ctypes.c_int32), ("slow_factor", ctypes.c_double),
+                ("slow_prob", ctypes.c_double)]
 
 
 _c_void_p, _i32, _i64, _u64, _f32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
@@ -137,9 +139,10 @@ def _w32(W, n):
 
 # ------------------------------------------------------------------ host calls
 def sample_mask(seed: int, step: int, n: int, m: int, kind: int, base: float = 1.0,
-                param: float = 1.0, slow_learner: int = -1, slow_factor: float = 1.0):
+                param: float = 1.0, slow_learner: int = -1, slow_factor: float = 1.0,
+                slow_prob: float = 0.0):
     """Returns (mask uint8[n, m], counts int32[n], times f64[n, m], timing f64[3])."""
-    d = Delay(kind, base, param, slow_learner, slow_factor)
+    d = Delay(kind, base, param, slow_learner, slow_factor, slow_prob)
     mask = np.zeros((max(n, 0), max(m, 0)), np.uint8)
     counts = np.zeros(max(n, 0), np.int32)
     times = np.zeros((max(n, 0), max(m, 0)), np.float64)

@@ -70,7 +70,13 @@ constexpr uint64_t kMul1 = 0xCA5A826395121157ull;
 constexpr uint64_t kBump0 = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kBump1 = 0xBB67AE8584CAA73Bull;
 
-enum : uint64_t { kPurposeDelay = 1, kPurposeGraph = 2, kPurposeActivation = 3, kPurposeShuffle = 4 };
+enum : uint64_t {
+  kPurposeDelay = 1,
+  kPurposeGraph = 2,
+  kPurposeActivation = 3,
+  kPurposeShuffle = 4,
+  kPurposeSlowdown = 5
+};
 
 struct Philox4x64 {
   uint64_t v[4];
@@ -124,12 +130,22 @@ extern "C" nbsgd_status nbsgd_sample_mask(uint64_t seed, uint64_t step, int32_t 
   if (d->kind != NBSGD_DELAY_CONST && !(d->param > 0.0))
     return fail(NBSGD_E_ARG, "delay param %g must be > 0", d->param);
   if (!(d->base >= 0.0) || !isfinite(d->base)) return fail(NBSGD_E_ARG, "delay base must be >= 0");
+  if (d->slow_learner < NBSGD_SLOW_RANDOM || d->slow_learner >= n)
+    return fail(NBSGD_E_ARG, "slow_learner=%d must be in [-2, n)", d->slow_learner);
   if (d->slow_learner >= 0 && !(d->slow_factor > 0.0))
     return fail(NBSGD_E_ARG, "slow_factor %g must be > 0", d->slow_factor);
+  if (d->slow_learner == NBSGD_SLOW_RANDOM &&
+      (!(d->slow_factor >= 1.0) || !isfinite(d->slow_factor) || !(d->slow_prob >= 0.0) ||
+       !(d->slow_prob <= 1.0)))
+    return fail(NBSGD_E_ARG, "random slow-down needs slow_factor >= 1 and slow_prob in [0, 1]");
 
   double finish[NBSGD_MAX_LEARNERS][NBSGD_MAX_MINIBATCHES];
   for (int32_t i = 0; i < n; ++i) {
-    const double s = (i == d->slow_learner) ? d->slow_factor : 1.0;
+    double s = (i == d->slow_learner) ? d->slow_factor : 1.0;
+    if (d->slow_learner == NBSGD_SLOW_RANDOM) {
+      const Philox4x64 b = philox(step, (uint64_t)i, 0, 0, seed, kPurposeSlowdown);
+      if (open_unit(b.v[0]) < d->slow_prob) s = 1.0 + (d->slow_factor - 1.0) * open_unit(b.v[1]);
+    }
     double clock = 0.0;
     for (int32_t j = 0; j < m; ++j) {
       const double u = open_unit(draw(seed, kPurposeDelay, step, (uint64_t)i, (uint64_t)j));

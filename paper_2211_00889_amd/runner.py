@@ -44,12 +44,13 @@ class Schedule:
 
     def __init__(self, wl):
         d = wl.delay
-        self.args = (wl.n, wl.m, _DELAY[d.kind], d.base, d.param, d.slow_learner, d.slow_factor)
+        self.args = (wl.n, wl.m, _DELAY[d.kind], d.base, d.param, d.slow_learner, d.slow_factor,
+                     d.slow_prob)
         self.seed = wl.seed
 
     def mask(self, step: int):
-        n, m, kind, base, param, slow, factor = self.args
-        return _lib.sample_mask(self.seed, step, n, m, kind, base, param, slow, factor)
+        n, m, kind, base, param, slow, factor, prob = self.args
+        return _lib.sample_mask(self.seed, step, n, m, kind, base, param, slow, factor, prob)
 
 
 class StepRunner:
@@ -131,16 +132,26 @@ class MlpRunner:
         self.order = _ORDER[wl.order]
         self.w_mean = _lib.w_allreduce(wl.n)
 
-    def step(self, k: int, stream=None):
-        """Iteration k; returns (mask, counts).  The finished mini-batches'
+    def step(self, k: int, stream=None, blocking: bool = False):
+        """Iteration k; returns (mask, counts, seconds): the finished mask, the
+        finished counts and the iteration's simulated wall time.  Non-blocking
+        (Alg. 2): the schedule's mask, time T_step (the terminal signal, or a
+        forced first mini-batch if later).  ``blocking``: the D-PSGD baseline
+        on the same W, every learner finishes all m mini-batches and the
+        iteration waits for the slowest, T_sync.  The finished mini-batches'
         losses are left in ``self.losses`` (index i*m + j)."""
         wl = self.wl
-        mask, counts, _, _ = self.schedule.mask(k)
+        mask, counts, _, timing = self.schedule.mask(k)
+        seconds = float(timing[2])
+        if blocking:
+            mask = np.ones_like(mask)
+            counts = np.full_like(counts, wl.m)
+            seconds = float(timing[1])
         idx = _lib.minibatch_indices(wl.seed, k, wl.n, wl.m, wl.batch, wl.shard)
         _lib.mlp_grad(self.X, wl.m, self.dims, self.data, self.labels, idx, mask, self.G, self.losses,
                       self.workspace, stream)
         _lib.step(self.X, self.V, self.G, mask, self.mixer.w(k), wl.lr, wl.momentum, self.order, stream)
-        return mask, counts
+        return mask, counts, seconds
 
     def evaluate(self, stream=None):
         """Loss of the average replica (the method's output) on the fixed

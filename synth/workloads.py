@@ -27,8 +27,9 @@ class DelaySpec:
     kind: str = "exp"          # "const" | "exp" | "lomax"
     base: float = 1.0
     param: float = 1.0         # exp: rate; lomax: shape
-    slow_learner: int = -1
+    slow_learner: int = -1     # -1: none; -2: random per iteration
     slow_factor: float = 1.0
+    slow_prob: float = 0.0     # random slow-down only
 
 
 @dataclass(frozen=True)
@@ -117,3 +118,11 @@ class MlpWorkload:
 MLP = MlpWorkload("mlp_n8_m8_b32_3072x512x10_ring")
 MLP_TINY = MlpWorkload("mlp_tiny_n4_m4_b32_128x64x10_ring", n=4, m=4, d_in=128, hidden=64,
                        n_samples=4 * 640, steps=12, eval_every=4, eval_samples=256, eval_stride=10)
+
+
+# The paper's heterogeneity model (Sec. 6.1): every iteration a random subset
+# of learners is slowed by a random factor, the slowest taking up to twice as
+# long as the fastest; mini-batch compute time otherwise constant.
+MLP_HETERO = replace(MLP, name="mlp_n8_m8_b32_3072x512x10_ring_random_slowdown",
+                     delay=DelaySpec("const", 1.0, 0.0, slow_learner=-2, slow_factor=2.0,
+                                     slow_prob=0.5))

@@ -32,7 +32,8 @@ def rel_err(got, want) -> float:
 
 def oracle_delay(wl):
     d = wl.delay
-    return oracle.schedule.Delay(ORACLE_DELAY[d.kind], d.base, d.param, d.slow_learner, d.slow_factor)
+    return oracle.schedule.Delay(ORACLE_DELAY[d.kind], d.base, d.param, d.slow_learner, d.slow_factor,
+                                 d.slow_prob)
 
 
 class OracleMixer:

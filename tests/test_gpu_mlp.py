@@ -91,7 +91,7 @@ def test_training_small_shape_matches_oracle(tiny):
     r = runner.MlpRunner(wl, DEV, A, y, x0)
     step_loss, counts = [], []
     for k in range(wl.steps):
-        mask, c = r.step(k)
+        mask, c, _ = r.step(k)
         L = r.losses.cpu().numpy().reshape(wl.n, wl.m)
         step_loss.append(np.mean([L[i][mask[i] > 0].mean() for i in range(wl.n)]))
         counts.append(c)
@@ -136,7 +136,7 @@ def test_full_workload_trajectory_matches_golden():
     for k in range(wl.steps):
         if k % wl.eval_every == 0:
             ev_loss.append(float(r.evaluate().mean().cpu()))
-        mask, c = r.step(k)
+        mask, c, _ = r.step(k)
         L = r.losses.cpu().numpy().reshape(wl.n, wl.m)
         step_loss.append(np.mean([L[i][mask[i] > 0].mean() for i in range(wl.n)]))
         counts.append(c)
@@ -165,3 +165,29 @@ def test_full_workload_trajectory_matches_golden():
         moved = np.sqrt(np.mean((ref["X"][:, sel] - x0s[:, sel]) ** 2))
         print(f"final X block {name}: gpu-oracle rms {gap:.3e}, training displacement rms {moved:.3e}")
         assert gap <= 0.1 * moved, name
+
+
+def test_blocking_baseline_small_shape_matches_oracle(tiny):
+    """The D-PSGD baseline (every mini-batch finished, iteration time T_sync)
+    on the same kernels, against the oracle's blocking run."""
+    wl, A, y, x0 = tiny
+    wl = dataclasses.replace(wl, delay=workloads.DelaySpec("const", 1.0, 0.0, slow_learner=-2,
+                                                           slow_factor=2.0, slow_prob=0.5))
+    _say(f"mlp blocking baseline {wl.name}")
+    r = runner.MlpRunner(wl, DEV, A, y, x0)
+    secs, step_loss = [], []
+    for k in range(wl.steps):
+        mask, c, t = r.step(k, blocking=True)
+        assert mask.all() and (c == wl.m).all()
+        L = r.losses.cpu().numpy()
+        step_loss.append(np.mean([L[i * wl.m:(i + 1) * wl.m].mean() for i in range(wl.n)]))
+        secs.append(t)
+    torch.cuda.synchronize()
+    ref = oracle.mlp.train(wl, A, y, x0, wl.steps, blocking=True)
+    assert secs == ref["seconds"]  # bitwise: same fp64 schedule on both sides
+    np.testing.assert_allclose(step_loss, ref["step_loss"], rtol=TOL_BF16)
+    blocks = mlp_blocks(*r.dims)
+    assert rel_err_blocks(r.X.cpu().numpy(), ref["X"], blocks) <= TOL_BF16
+    # the non-blocking schedule of the same iterations is never slower
+    nb_secs = [runner.Schedule(wl).mask(k)[3][2] for k in range(wl.steps)]
+    assert all(a <= b for a, b in zip(nb_secs, secs))

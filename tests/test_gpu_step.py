@@ -242,3 +242,27 @@ def test_gpu_argument_errors():
         nb.step(V, V, G, np.ones((n, m)), nb.w_ring(n), 0.1, 0.9, 0)
     assert e.value.status == _lib.E_ARG
     torch.cuda.synchronize()
+
+
+def test_parameter_server_variant():
+    """Alg. 3 (with 1/n): the fused step-then-mix kernel with uniform W on
+    replicas that all hold the server model, over several iterations."""
+    n, m, P = 6, 5, 40003
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal(P).astype(np.float32)
+    G = (0.03 * rng.standard_normal((n, m, P))).astype(np.float32)
+    Xd = _dev(np.tile(x, (n, 1)))
+    Vd = torch.zeros(n, P, dtype=torch.float32, device=DEV)
+    Gd = _dev(G)
+    xo, Vo = x.astype(np.float64), np.zeros((n, P))
+    for k in range(4):
+        mask = _random_mask(rng, n, m)
+        _say(f"parameter server iteration {k}")
+        nb.step(Xd, Vd, Gd, mask, nb.w_allreduce(n), 0.2, 0.9, nb.STEP_THEN_MIX)
+        xo, Vo = oracle.step.parameter_server_step(xo, Vo, G, mask, float(np.float32(0.2)),
+                                                   float(np.float32(0.9)))
+    torch.cuda.synchronize()
+    out = Xd.cpu().numpy()
+    assert all(np.array_equal(out[0], out[i]) for i in range(n))
+    assert rel_err(out[0], xo) <= TOL
+    assert rel_err(Vd.cpu().numpy(), Vo) <= TOL

@@ -32,24 +32,27 @@ def test_exports_every_declared_symbol():
 
 
 DELAYS = [
-    (nb.DELAY_EXP, 1.0, 1.0, -1, 1.0),
-    (nb.DELAY_EXP, 1.0, 1.0, 7, 3.0),
-    (nb.DELAY_EXP, 1.0, 0.5, -1, 1.0),
-    (nb.DELAY_LOMAX, 1.0, 1.5, -1, 1.0),
-    (nb.DELAY_CONST, 1.0, 0.0, -1, 1.0),
-    (nb.DELAY_EXP, 0.0, 2.0, 0, 1e9),
+    (nb.DELAY_EXP, 1.0, 1.0, -1, 1.0, 0.0),
+    (nb.DELAY_EXP, 1.0, 1.0, 7, 3.0, 0.0),
+    (nb.DELAY_EXP, 1.0, 0.5, -1, 1.0, 0.0),
+    (nb.DELAY_LOMAX, 1.0, 1.5, -1, 1.0, 0.0),
+    (nb.DELAY_CONST, 1.0, 0.0, -1, 1.0, 0.0),
+    (nb.DELAY_EXP, 0.0, 2.0, 0, 1e9, 0.0),
+    (nb.DELAY_EXP, 1.0, 1.0, -2, 2.0, 0.5),    # per-iteration random slow-down
+    (nb.DELAY_CONST, 1.0, 0.0, -2, 2.0, 0.3),
 ]
 
 
 @pytest.mark.parametrize("delay", DELAYS)
 @pytest.mark.parametrize("n,m", [(1, 1), (4, 4), (8, 8), (16, 4), (8, 16), (3, 64)])
 def test_sample_mask_bitwise(delay, n, m):
-    kind, base, param, slow, factor = delay
+    kind, base, param, slow, factor, prob = delay
     if slow >= n:
         slow = n - 1
-    d = Delay(kind, base, param, slow, factor)
+    d = Delay(kind, base, param, slow, factor, prob)
     for seed, step in ((0, 0), (0, 1), (0, 49), (12345, 7)):
-        mask, counts, times, timing = nb.sample_mask(seed, step, n, m, kind, base, param, slow, factor)
+        mask, counts, times, timing = nb.sample_mask(seed, step, n, m, kind, base, param, slow, factor,
+                                                     prob)
         s = oracle.schedule.sample_schedule(seed, step, n, m, d)
         assert np.array_equal(mask, s["mask"])
         assert np.array_equal(counts, s["counts"])
@@ -97,6 +100,10 @@ def test_host_errors():
     with pytest.raises(nb.NbsgdError) as e:
         nb.Matcha(0, 5, 3)
     assert e.value.status == _lib.E_SHAPE
+    for slow, factor, prob in ((4, 2.0, 0.0), (-3, 2.0, 0.0), (-2, 0.5, 0.5), (-2, 2.0, 1.5)):
+        with pytest.raises(nb.NbsgdError) as e:
+            nb.sample_mask(0, 0, 4, 4, nb.DELAY_EXP, 1.0, 1.0, slow, factor, prob)
+        assert e.value.status == _lib.E_ARG
     lib = _lib.load()
     assert lib.nbsgd_sample_mask(0, 0, 4, 4, None, None, None, None, None) == _lib.E_ARG
     assert b"null" in lib.nbsgd_last_error()

@@ -100,3 +100,23 @@ def test_deterministic_in_seed_and_step():
     c = schedule.sample_schedule(11, 5, 4, 4, d)
     assert np.array_equal(a["times"], b["times"])
     assert not np.array_equal(a["times"], c["times"])
+
+
+def test_random_slowdown_model():
+    # Sec. 6.1 heterogeneity: slowed nodes and slow-down rates change every
+    # iteration, the slowest taking up to twice as long as the fastest
+    from oracle.schedule import SLOW_RANDOM
+
+    d = Delay(DELAY_CONST, base=1.0, slow_learner=SLOW_RANDOM, slow_factor=2.0, slow_prob=0.5)
+    scales = np.array([[schedule.slowdown(3, k, i, d) for i in range(8)] for k in range(3000)])
+    slowed = scales > 1.0
+    assert abs(slowed.mean() - 0.5) < 4 * 0.5 / math.sqrt(scales.size)
+    assert scales.min() >= 1.0 and scales.max() < 2.0
+    s = scales[slowed]
+    assert abs(s.mean() - 1.5) < 4 * (1 / math.sqrt(12)) / math.sqrt(s.size)  # uniform on (1, 2)
+    # the slowed set changes between iterations
+    assert not all(np.array_equal(slowed[k], slowed[k + 1]) for k in range(20))
+    # with constant base times a learner's mini-batch time is exactly its scale
+    sch = schedule.sample_schedule(3, 5, 8, 4, d)
+    np.testing.assert_array_equal(sch["times"][:, 0], scales[5])
+    assert sch["times"].max() / sch["times"].min() < 2.0

@@ -172,3 +172,22 @@ def test_brute_force_all_masks_tiny():
                         x = sum(W[i, p] * (X[p, e] - eta[p] * v[p]) for p in range(n))
                     assert Xn[i, e] == pytest.approx(x, abs=1e-14)
                     assert Vn[i, e] == pytest.approx(v[i], abs=1e-15)
+
+
+def test_parameter_server_equals_uniform_step_then_mix_from_identical_replicas():
+    # Alg. 3 (with 1/n) is the uniform-W step-then-mix iteration when every
+    # learner starts from the server model: x' = mean_i (x - eta_i v_i').
+    n, m, P = 5, 4, 7
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal(P)
+    V = rng.standard_normal((n, P)) * 0.1
+    G = rng.standard_normal((n, m, P)) * 0.05
+    mask = _random_prefix_mask(rng, n, m)
+    xp, Vp = step.parameter_server_step(x, V, G, mask, 0.3, 0.8)
+    Xs, Vs = step.step(np.tile(x, (n, 1)), V, G, mask, mixing.w_uniform(n), 0.3, 0.8, STEP_THEN_MIX)
+    np.testing.assert_allclose(Xs, np.broadcast_to(xp, Xs.shape), atol=1e-14)
+    np.testing.assert_array_equal(Vp, Vs)
+    # one learner, no momentum: plain SGD with the finished-fraction rate
+    x1, _ = step.parameter_server_step(x, np.zeros((1, P)), G[:1], mask[:1], 0.3, 0.0)
+    c = int(mask[0].sum())
+    np.testing.assert_allclose(x1, x - 0.3 * (c / m) * G[0, :c].mean(axis=0), atol=1e-15)
