@@ -184,16 +184,17 @@ nbsgd_status nbsgd_step(float *X, float *V, const float *G, const uint8_t *mask,
 nbsgd_status nbsgd_w_allreduce(int32_t n, float *W);
 nbsgd_status nbsgd_w_ring(int32_t n, float *W);
 
-/* MATCHA with communication budget 1/2 (Sec. 6.1): a random `degree`-regular
+/* MATCHA with a communication budget (Sec. 6.1): a random `degree`-regular
  * simple connected base graph on n nodes (pairing model; half-edge shuffle by
  * Fisher-Yates from the top with Philox4x64-10 word 0 at counter
  * (attempt, position, 0, 0) under key (seed, 2) mapped to [0, t] by
  * floor(w * (t+1) / 2^64); rejected and redrawn on a loop, a repeated edge or
  * a disconnected graph), split into matchings by greedy edge colouring in
- * lexicographic edge order.  At iteration `step` matching q is active iff the
- * top bit of Philox word 0 at counter (step, q, 0, 0) under key (seed, 3) is
- * 0, and W = I - alpha * sum_{active q} L_q, L_q the Laplacian of matching q,
- * alpha = 1 / (degree + 1).
+ * lexicographic edge order.  At iteration `step` matching q is active iff
+ * u < p_q, u = ((w >> 12) + 0.5) * 2^-52 from Philox word 0 at counter
+ * (step, q, 0, 0) under key (seed, 3), and W = I - alpha * sum_{active q} L_q,
+ * L_q the Laplacian of matching q.  By default every p_q = 1/2 (budget 0.5)
+ * and alpha = 1 / (degree + 1).
  * nbsgd_matcha_create: builds the graph; *out is owned by the caller and
  *   released with nbsgd_matcha_destroy.  Errors: NBSGD_E_ARG, NBSGD_E_SHAPE
  *   (no such regular graph), NBSGD_E_UNSUPPORTED.
@@ -201,12 +202,25 @@ nbsgd_status nbsgd_w_ring(int32_t n, float *W);
  *   number of active matchings.
  * nbsgd_matcha_matchings: edges_uvq int32[3*E] as (u, v, matching) with u < v
  *   in lexicographic order (nullable to query sizes), *E edges, *M matchings.
- */
+ * nbsgd_matcha_set / nbsgd_matcha_get: the activation probabilities p[M] (each
+ *   in [0, 1]) and alpha (in (0, 1/degree], so W stays non-negative).
+ * nbsgd_matcha_optimize: MATCHA's own choice under budget b in (0, 1]: p
+ *   maximising the algebraic connectivity lambda_2(sum_q p_q L_q) subject to
+ *   0 <= p_q <= 1 and sum_q p_q <= b * M (projected supergradient ascent,
+ *   `iterations` steps, the best iterate kept), then alpha minimising the
+ *   spectral norm of E[W^T W] - J/n = I - J/n - 2 alpha Lbar
+ *   + alpha^2 (Lbar^2 + 2 sum_q p_q (1 - p_q) L_q) over (0, 1/degree]
+ *   (grid, then golden section).  lambda2 and spectral (nullable) receive the
+ *   attained values.  Host only, O(iterations * n^3).                        */
 typedef struct nbsgd_matcha nbsgd_matcha;
 nbsgd_status nbsgd_matcha_create(uint64_t seed, int32_t n, int32_t degree, nbsgd_matcha **out);
 nbsgd_status nbsgd_matcha_w(const nbsgd_matcha *g, uint64_t step, float *W, int32_t *n_active);
 nbsgd_status nbsgd_matcha_matchings(const nbsgd_matcha *g, int32_t *edges_uvq, int32_t *E,
                                     int32_t *M);
+nbsgd_status nbsgd_matcha_set(nbsgd_matcha *g, const double *probs, double alpha);
+nbsgd_status nbsgd_matcha_get(const nbsgd_matcha *g, double *probs, double *alpha);
+nbsgd_status nbsgd_matcha_optimize(nbsgd_matcha *g, double budget, int32_t iterations,
+                                   double *lambda2, double *spectral);
 void nbsgd_matcha_destroy(nbsgd_matcha *g);
 
 /* -------------------------------------------------- end-to-end MLP workload

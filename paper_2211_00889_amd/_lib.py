@@ -25,7 +25,8 @@ SLOW_NONE, SLOW_RANDOM = -1, -2
 
 EXPORTS = ("nbsgd_sample_mask", "nbsgd_accumulate", "nbsgd_mix", "nbsgd_update", "nbsgd_step",
            "nbsgd_w_allreduce", "nbsgd_w_ring", "nbsgd_matcha_create", "nbsgd_matcha_w",
-           "nbsgd_matcha_matchings", "nbsgd_matcha_destroy", "nbsgd_mlp_param_count",
+           "nbsgd_matcha_matchings", "nbsgd_matcha_set", "nbsgd_matcha_get", "nbsgd_matcha_optimize",
+           "nbsgd_matcha_destroy", "nbsgd_mlp_param_count",
            "nbsgd_mlp_workspace_bytes", "nbsgd_minibatch_indices", "nbsgd_mlp_grad",
            "nbsgd_mlp_loss", "nbsgd_last_error")
 
@@ -73,6 +74,9 @@ def load():
         "nbsgd_matcha_create": [_u64, _i32, _i32, ctypes.POINTER(_c_void_p)],
         "nbsgd_matcha_w": [_c_void_p, _u64, _c_void_p, _c_void_p],
         "nbsgd_matcha_matchings": [_c_void_p, _c_void_p, _c_void_p, _c_void_p],
+        "nbsgd_matcha_set": [_c_void_p, _c_void_p, ctypes.c_double],
+        "nbsgd_matcha_get": [_c_void_p, _c_void_p, _c_void_p],
+        "nbsgd_matcha_optimize": [_c_void_p, ctypes.c_double, _i32, _c_void_p, _c_void_p],
         "nbsgd_mlp_param_count": [ctypes.POINTER(MlpShape), ctypes.POINTER(_i64)],
         "nbsgd_mlp_workspace_bytes": [ctypes.POINTER(MlpShape), _i64, ctypes.POINTER(ctypes.c_size_t)],
         "nbsgd_minibatch_indices": [_u64, _u64, _i32, _i32, _i32, _i32, _c_void_p],
@@ -186,6 +190,25 @@ class Matcha:
         _check(load().nbsgd_matcha_matchings(self._h, _host_ptr(buf), ctypes.byref(E),
                                              ctypes.byref(M)))
         return buf, M.value
+
+    def set(self, probs, alpha: float):
+        probs = np.ascontiguousarray(np.asarray(probs), dtype=np.float64)
+        _check(load().nbsgd_matcha_set(self._h, _host_ptr(probs), float(alpha)))
+
+    def get(self):
+        _, M = self.matchings()
+        probs = np.zeros(M, np.float64)
+        alpha = ctypes.c_double(0.0)
+        _check(load().nbsgd_matcha_get(self._h, _host_ptr(probs), ctypes.byref(alpha)))
+        return probs, alpha.value
+
+    def optimize(self, budget: float, iterations: int = 2000):
+        """MATCHA's own activation probabilities and alpha; returns
+        (lambda_2, spectral norm) attained."""
+        l2, rho = ctypes.c_double(0.0), ctypes.c_double(0.0)
+        _check(load().nbsgd_matcha_optimize(self._h, budget, iterations, ctypes.byref(l2),
+                                            ctypes.byref(rho)))
+        return l2.value, rho.value
 
     def close(self):
         if getattr(self, "_h", None):

@@ -48,14 +48,17 @@ def build(verbose: bool = False) -> None:
     host_o = os.path.join(OBJ, "host.o")
     _run([cxx, *CXX_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "host.cpp"),
           "-o", host_o], verbose)
+    matcha_o = os.path.join(OBJ, "matcha.o")
+    _run([cxx, *CXX_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "matcha.cpp"),
+          "-o", matcha_o], verbose)
     step_o = os.path.join(OBJ, "step.o")
     _run([HIPCC, *HIP_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "step.hip"),
           "-o", step_o], verbose)
     mlp_o = os.path.join(OBJ, "mlp.o")
     _run([HIPCC, *HIP_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "mlp.hip"),
           "-o", mlp_o], verbose)
-    _atomic_link([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", host_o, step_o, mlp_o], LIB,
-                 verbose)
+    _atomic_link([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", host_o, matcha_o, step_o, mlp_o],
+                 LIB, verbose)
     _atomic_link([HIPCC, *HIP_FLAGS, "-shared", os.path.join(ROOT, "synth", "fill.hip")],
                  SYNTH_LIB, verbose)
 

@@ -70,13 +70,6 @@ constexpr uint64_t kMul1 = 0xCA5A826395121157ull;
 constexpr uint64_t kBump0 = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kBump1 = 0xBB67AE8584CAA73Bull;
 
-enum : uint64_t {
-  kPurposeDelay = 1,
-  kPurposeGraph = 2,
-  kPurposeActivation = 3,
-  kPurposeShuffle = 4,
-  kPurposeSlowdown = 5
-};
 
 struct Philox4x64 {
   uint64_t v[4];
@@ -101,19 +94,16 @@ Philox4x64 philox(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3, uint64_t k
   return Philox4x64{{c0, c1, c2, c3}};
 }
 
-inline uint64_t draw(uint64_t seed, uint64_t purpose, uint64_t c0, uint64_t c1, uint64_t c2) {
+}  // namespace
+
+uint64_t draw(uint64_t seed, uint64_t purpose, uint64_t c0, uint64_t c1, uint64_t c2) {
   return philox(c0, c1, c2, 0, seed, purpose).v[0];
 }
 
-// (0,1): 52 random bits plus one half unit, exact in fp64.
-inline double open_unit(uint64_t w) { return ((double)(w >> 12) + 0.5) * 0x1p-52; }
+double open_unit(uint64_t w) { return ((double)(w >> 12) + 0.5) * 0x1p-52; }
 
-// [0, k) by multiply-shift.
-inline uint64_t below(uint64_t w, uint64_t k) {
-  return (uint64_t)(((unsigned __int128)w * k) >> 64);
-}
+uint64_t below(uint64_t w, uint64_t k) { return (uint64_t)(((unsigned __int128)w * k) >> 64); }
 
-}  // namespace
 }  // namespace nbsgd
 
 using namespace nbsgd;
@@ -205,137 +195,7 @@ extern "C" nbsgd_status nbsgd_w_ring(int32_t n, float* W) {
   return NBSGD_OK;
 }
 
-struct nbsgd_matcha {
-  uint64_t seed;
-  int32_t n, degree, matchings;
-  double alpha;
-  std::vector<std::pair<int32_t, int32_t>> edges;  // u < v, lexicographic
-  std::vector<int32_t> colour;                     // matching of each edge
-};
 
-namespace {
-
-bool connected(int32_t n, const std::vector<std::pair<int32_t, int32_t>>& edges) {
-  std::vector<std::vector<int32_t>> adj(n);
-  for (auto& e : edges) {
-    adj[e.first].push_back(e.second);
-    adj[e.second].push_back(e.first);
-  }
-  std::vector<char> seen(n, 0);
-  std::vector<int32_t> todo{0};
-  seen[0] = 1;
-  int32_t reached = 1;
-  while (!todo.empty()) {
-    const int32_t u = todo.back();
-    todo.pop_back();
-    for (int32_t v : adj[u])
-      if (!seen[v]) {
-        seen[v] = 1;
-        ++reached;
-        todo.push_back(v);
-      }
-  }
-  return reached == n;
-}
-
-}  // namespace
-
-extern "C" nbsgd_status nbsgd_matcha_create(uint64_t seed, int32_t n, int32_t degree,
-                                            nbsgd_matcha** out) {
-  clear_error();
-  if (!out) return fail(NBSGD_E_ARG, "out is null");
-  *out = nullptr;
-  if (nbsgd_status st = check_nm(n, 1)) return st;
-  if (n < 2 || degree < 1 || degree >= n || (n * degree) % 2)
-    return fail(NBSGD_E_SHAPE, "no simple %d-regular graph on %d nodes", degree, n);
-  const int32_t H = n * degree;
-  std::vector<int32_t> half(H);
-  std::vector<std::pair<int32_t, int32_t>> edges;
-  bool found = false;
-  for (uint64_t attempt = 0; attempt < 100000 && !found; ++attempt) {
-    for (int32_t h = 0; h < H; ++h) half[h] = h;
-    for (int32_t t = H - 1; t >= 1; --t) {
-      const uint64_t r = below(draw(seed, kPurposeGraph, attempt, (uint64_t)t, 0), (uint64_t)t + 1);
-      std::swap(half[t], half[r]);
-    }
-    std::set<std::pair<int32_t, int32_t>> es;
-    bool ok = true;
-    for (int32_t k = 0; k < H && ok; k += 2) {
-      const int32_t u = half[k] / degree, v = half[k + 1] / degree;
-      if (u == v) ok = false;
-      else ok = es.insert({std::min(u, v), std::max(u, v)}).second;
-    }
-    if (!ok) continue;
-    edges.assign(es.begin(), es.end());  // std::set orders lexicographically
-    found = connected(n, edges);
-  }
-  if (!found) return fail(NBSGD_E_SHAPE, "pairing model found no connected simple graph");
-
-  nbsgd_matcha* g = new (std::nothrow) nbsgd_matcha;
-  if (!g) return fail(NBSGD_E_ARG, "out of host memory");
-  g->seed = seed;
-  g->n = n;
-  g->degree = degree;
-  g->alpha = 1.0 / (double)(degree + 1);
-  g->edges = edges;
-  g->colour.assign(edges.size(), 0);
-  std::vector<std::set<int32_t>> used(n);
-  int32_t M = 0;
-  for (size_t k = 0; k < edges.size(); ++k) {
-    const int32_t u = edges[k].first, v = edges[k].second;
-    int32_t c = 0;
-    while (used[u].count(c) || used[v].count(c)) ++c;
-    g->colour[k] = c;
-    used[u].insert(c);
-    used[v].insert(c);
-    M = std::max(M, c + 1);
-  }
-  g->matchings = M;
-  *out = g;
-  return NBSGD_OK;
-}
-
-extern "C" nbsgd_status nbsgd_matcha_w(const nbsgd_matcha* g, uint64_t step, float* W,
-                                       int32_t* n_active) {
-  clear_error();
-  if (!g || !W) return fail(NBSGD_E_ARG, "g and W must not be null");
-  const int32_t n = g->n;
-  std::vector<double> acc((size_t)n * n, 0.0);
-  for (int32_t i = 0; i < n; ++i) acc[(size_t)i * n + i] = 1.0;
-  int32_t active = 0;
-  for (int32_t q = 0; q < g->matchings; ++q) {
-    if ((draw(g->seed, kPurposeActivation, step, (uint64_t)q, 0) >> 63) != 0) continue;
-    ++active;
-    for (size_t k = 0; k < g->edges.size(); ++k) {
-      if (g->colour[k] != q) continue;
-      const int32_t u = g->edges[k].first, v = g->edges[k].second;
-      acc[(size_t)u * n + u] -= g->alpha;
-      acc[(size_t)v * n + v] -= g->alpha;
-      acc[(size_t)u * n + v] += g->alpha;
-      acc[(size_t)v * n + u] += g->alpha;
-    }
-  }
-  for (size_t k = 0; k < acc.size(); ++k) W[k] = (float)acc[k];
-  if (n_active) *n_active = active;
-  return NBSGD_OK;
-}
-
-extern "C" nbsgd_status nbsgd_matcha_matchings(const nbsgd_matcha* g, int32_t* edges_uvq,
-                                               int32_t* E, int32_t* M) {
-  clear_error();
-  if (!g || !E || !M) return fail(NBSGD_E_ARG, "g, E and M must not be null");
-  *E = (int32_t)g->edges.size();
-  *M = g->matchings;
-  if (edges_uvq)
-    for (size_t k = 0; k < g->edges.size(); ++k) {
-      edges_uvq[3 * k + 0] = g->edges[k].first;
-      edges_uvq[3 * k + 1] = g->edges[k].second;
-      edges_uvq[3 * k + 2] = g->colour[k];
-    }
-  return NBSGD_OK;
-}
-
-extern "C" void nbsgd_matcha_destroy(nbsgd_matcha* g) { delete g; }
 
 extern "C" const char* nbsgd_last_error(void) { return g_error.c_str(); }
 

@@ -21,7 +21,7 @@ _ORDER = {"mix_then_step": MIX_THEN_STEP, "step_then_mix": STEP_THEN_MIX}
 class Mixer:
     """Per-iteration mixing matrix of a workload's kind."""
 
-    def __init__(self, kind: str, n: int, seed: int, degree: int = 3):
+    def __init__(self, kind: str, n: int, seed: int, degree: int = 3, budget=None):
         self.kind = kind
         self.matcha = None
         if kind == "uniform":
@@ -30,6 +30,8 @@ class Mixer:
             self.fixed = _lib.w_ring(n)
         elif kind == "matcha":
             self.matcha = _lib.Matcha(seed, n, degree)
+            if budget is not None:  # MATCHA's optimised probabilities and alpha
+                self.matcha.optimize(budget)
         else:
             raise ValueError(f"unknown mixing kind {kind}")
 
@@ -73,7 +75,7 @@ class StepRunner:
             synth_device.fill_normal(self.X, wl.seed, workloads.STREAM_X, wl.x_std)
             synth_device.fill_normal(self.G, wl.seed, workloads.STREAM_G, wl.g_std)
         self.order = _ORDER[wl.order]
-        self.mixer = Mixer(wl.mixing, n, wl.seed, wl.matcha_degree)
+        self.mixer = Mixer(wl.mixing, n, wl.seed, wl.matcha_degree, wl.matcha_budget)
         self.schedule = Schedule(wl)
 
     def plan(self, step: int):

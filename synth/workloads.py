@@ -48,6 +48,7 @@ class Workload:
     x_std: float = 1.0
     g_std: float = math.sqrt(1e-3)   # N(0, 1e-3) read as variance 1e-3
     matcha_degree: int = 3
+    matcha_budget: float | None = None   # set: MATCHA's optimised p and alpha under this budget
     notes: str = ""
     extra: dict = field(default_factory=dict)
 
@@ -69,9 +70,13 @@ RESNET50_MATCHA = Workload("resnet50_n16_m4_P23.5M_matcha", 16, 4, 23_500_000, "
 VGG16_ALLREDUCE = Workload("vgg16_n8_m16_P138M_allreduce", 8, 16, 138_000_000, "uniform",
                            STEP_THEN_MIX, DelaySpec("lomax", 1.0, 1.5), 0.05, 0.9, 20)
 
-WORKLOADS = {w.name: w for w in (TINY, RESNET18_RING, RESNET50_MATCHA, VGG16_ALLREDUCE)}
+RESNET50_MATCHA_OPT = replace(RESNET50_MATCHA, name="resnet50_n16_m4_P23.5M_matcha_optimised",
+                              matcha_budget=0.5)
+
+WORKLOADS = {w.name: w for w in (TINY, RESNET18_RING, RESNET50_MATCHA, VGG16_ALLREDUCE,
+                                 RESNET50_MATCHA_OPT)}
 ALIASES = {"tiny": TINY.name, "resnet18": RESNET18_RING.name, "resnet50": RESNET50_MATCHA.name,
-           "vgg16": VGG16_ALLREDUCE.name}
+           "vgg16": VGG16_ALLREDUCE.name, "resnet50opt": RESNET50_MATCHA_OPT.name}
 
 
 def get(name: str) -> Workload:

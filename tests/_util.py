@@ -41,6 +41,8 @@ class OracleMixer:
         self.wl = wl
         self.matcha = oracle.mixing.Matcha(wl.seed, wl.n, wl.matcha_degree) \
             if wl.mixing == "matcha" else None
+        if self.matcha is not None and wl.matcha_budget is not None:
+            self.matcha.optimize(wl.matcha_budget)
 
     def w(self, step):
         """The oracle's W, stored in the ABI's fp32 and widened back to fp64."""

@@ -206,7 +206,7 @@ def _windows(P, seed, k=8, width=4096, edge=65536):
     return np.unique(np.concatenate(cols))
 
 
-@pytest.mark.parametrize("name", ["resnet18", "resnet50", "vgg16"])
+@pytest.mark.parametrize("name", ["resnet18", "resnet50", "vgg16", "resnet50opt"])
 def test_full_size_workload_sampled_columns(name):
     """Full-size workload, every iteration, bench launch configuration;
     compared on sampled column windows (first, last and random)."""

@@ -204,3 +204,53 @@ def test_mlp_grad_rejects_bad_indices_before_launch():
     rc = lib.nbsgd_mlp_grad(p, n, m, ctypes.byref(shape), p, p, 100, idx.ctypes.data_as(ctypes.c_void_p),
                             mask.ctypes.data_as(ctypes.c_void_p), p, p, p, ws - 1, None)
     assert rc == _lib.E_ARG and b"workspace" in lib.nbsgd_last_error()
+
+
+@pytest.mark.parametrize("seed,n,degree,budget", [(0, 16, 3, 0.5), (1, 10, 4, 0.3), (3, 12, 2, 1.0)])
+def test_matcha_optimize_matches_oracle(seed, n, degree, budget):
+    g = nb.Matcha(seed, n, degree)
+    o = oracle.mixing.Matcha(seed, n, degree)
+    lam, rho = g.optimize(budget, 1500)
+    lam_o, rho_o = o.optimize(budget, 1500)
+    probs, alpha = g.get()
+    M = len(probs)
+    assert (probs >= 0).all() and (probs <= 1).all() and probs.sum() <= budget * M + 1e-9
+    assert 0 < alpha <= 1.0 / degree
+    # the library's own figures, re-evaluated by the oracle at its p and alpha
+    assert o.connectivity(probs)[0] == pytest.approx(lam, abs=1e-10)
+    assert o.spectral(probs, alpha) == pytest.approx(rho, abs=1e-10)
+    # the same optimum (eigenvector bases may differ where lambda_2 is repeated)
+    assert lam == pytest.approx(lam_o, abs=1e-3)
+    assert rho == pytest.approx(rho_o, abs=1e-3)
+    # W at the optimised p and alpha, bitwise against the oracle given those values
+    o.probs, o.alpha = probs.tolist(), alpha
+    for step in range(40):
+        W, active = g.w(step)
+        assert np.array_equal(W, o.w(step).astype(np.float32))
+        assert active == sum(o.active(step))
+    g.close()
+
+
+def test_matcha_set_get_and_errors():
+    g = nb.Matcha(0, 16, 3)
+    probs, alpha = g.get()
+    assert (probs == 0.5).all() and alpha == 0.25
+    p = np.linspace(0.1, 0.9, len(probs))
+    g.set(p, 0.3)
+    p2, a2 = g.get()
+    assert np.array_equal(p2, p) and a2 == 0.3
+    o = oracle.mixing.Matcha(0, 16, 3)
+    o.probs, o.alpha = p.tolist(), 0.3
+    for step in range(20):
+        assert np.array_equal(g.w(step)[0], o.w(step).astype(np.float32))
+    for bad_p, bad_a in ((np.full(len(p), 1.5), 0.2), (np.full(len(p), -0.1), 0.2),
+                         (p, 0.0), (p, 0.34), (np.full(len(p), np.nan), 0.2)):
+        with pytest.raises(nb.NbsgdError) as e:
+            g.set(bad_p, bad_a)
+        assert e.value.status == _lib.E_ARG
+    assert np.array_equal(g.get()[0], p)  # a rejected call changes nothing
+    for budget, iters in ((0.0, 10), (1.5, 10), (0.5, 0)):
+        with pytest.raises(nb.NbsgdError) as e:
+            g.optimize(budget, iters)
+        assert e.value.status == _lib.E_ARG
+    g.close()
