@@ -228,14 +228,17 @@ void nbsgd_matcha_destroy(nbsgd_matcha *g);
  * softmax cross-entropy, on a data set split into n equal shards (Alg. 1/2
  * initialisation; Eq. 1 with the per-sample cross-entropy as l).
  * Flat parameter layout of one replica row: W1[d_in][hidden] row-major,
- * b1[hidden], W2[hidden][classes], b2[classes].
+ * b1[hidden], W2[hidden][classes], b2[classes], then zeros up to a multiple
+ * of 4 floats (so that every row of X, V and G starts 16-byte aligned and the
+ * fused step streams it in 16-byte vectors).
  * Supported shapes: batch == 32, d_in a multiple of 128, hidden a multiple of 64,
  * hidden <= 512, 2 <= classes <= 16 (NBSGD_E_UNSUPPORTED otherwise).        */
 typedef struct {
   int32_t d_in, hidden, classes, batch;
 } nbsgd_mlp_shape;
 
-/* Parameters per replica (d_in*hidden + hidden + hidden*classes + classes). */
+/* Parameters per replica: d_in*hidden + hidden + hidden*classes + classes,
+ * rounded up to a multiple of 4 (the padding). */
 nbsgd_status nbsgd_mlp_param_count(const nbsgd_mlp_shape *s, int64_t *P);
 
 /* Device workspace, in bytes, for calls that process up to `rows` sample rows:
@@ -251,7 +254,9 @@ nbsgd_status nbsgd_mlp_workspace_bytes(const nbsgd_mlp_shape *s, int64_t rows, s
  * word 0 at counter (e, i, t, 0) under key (seed, 4)); iteration `step` is
  * window step mod (shard / (m*b)) of epoch step div (shard / (m*b)), and
  * mini-batch j is the j-th run of b samples of that window.  Windows are
- * consumed whether or not their mini-batches finish.
+ * consumed whether or not their mini-batches finish.  The permutations of
+ * the last epoch asked for are kept per calling thread, so the iterations of
+ * an epoch after the first cost O(n*m*b).
  * idx: host int32 [n][m][b], global sample indices (caller-owned).
  * Errors: NBSGD_E_ARG (null idx), NBSGD_E_SHAPE (shard < m*b, b < 1),
  *         NBSGD_E_UNSUPPORTED.                                              */
@@ -264,15 +269,17 @@ nbsgd_status nbsgd_minibatch_indices(uint64_t seed, uint64_t step, int32_t n, in
  *   G[i][j][:] = gradient of the mean cross-entropy of the 32 samples
  *                idx[i][j][:] at parameters X[i], for mask[i*m+j] != 0;
  *   losses[i*m+j] = that mean loss.
- * Unfinished rows of G and entries of losses are left untouched.  Every GEMM
+ * The padding entries of a finished row are set to 0.  Unfinished rows of G
+ * and entries of losses are left untouched.  Every GEMM
  * input (the samples, W1, bf16(ReLU(Z1)), W2, dZ2, dZ1) is rounded to bf16
  * (nearest even) and multiplied on the matrix cores with fp32 accumulation;
  * bias, ReLU, softmax and cross-entropy are fp32.
  * X      device fp32 [n][P] (P from nbsgd_mlp_param_count)
  * data   device fp32 [n_samples][d_in]; labels device int32 [n_samples] in
  *        [0, classes) (values outside are clamped into range)
- * idx    host int32 [n*m*batch], every value in [0, n_samples) (NBSGD_E_ARG);
- *        read before the call returns (copied through kernel arguments)
+ * idx    host int32 [n*m*batch]; the entries of finished mini-batches must be
+ *        in [0, n_samples) (NBSGD_E_ARG, checked before any launch); read
+ *        before the call returns (copied through kernel arguments)
  * mask   host uint8 [n*m]
  * G      device fp32 [n][m][P]; losses device fp32 [n*m]
  * workspace  device, >= nbsgd_mlp_workspace_bytes(s, n*m*batch)

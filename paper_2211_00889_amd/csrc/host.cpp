@@ -200,6 +200,43 @@ extern "C" nbsgd_status nbsgd_w_ring(int32_t n, float* W) {
 extern "C" const char* nbsgd_last_error(void) { return g_error.c_str(); }
 
 // ------------------------------------------------------------ local shuffle
+namespace {
+
+// The permutations of the last epoch asked for on this thread: every
+// iteration of an epoch reads a window of the same permutations.
+struct EpochPerm {
+  bool valid = false;
+  uint64_t seed = 0, epoch = 0;
+  int32_t n = 0, shard = 0;
+  std::vector<int32_t> perm;  // [n][shard]
+};
+thread_local EpochPerm t_perm;
+
+const std::vector<int32_t>& epoch_permutations(uint64_t seed, uint64_t epoch, int32_t n,
+                                               int32_t shard) {
+  EpochPerm& e = t_perm;
+  if (e.valid && e.seed == seed && e.epoch == epoch && e.n == n && e.shard == shard) return e.perm;
+  e.valid = false;
+  e.perm.resize((size_t)n * shard);
+  for (int32_t i = 0; i < n; ++i) {
+    int32_t* perm = e.perm.data() + (size_t)i * shard;
+    for (int32_t t = 0; t < shard; ++t) perm[t] = t;
+    for (int32_t t = shard - 1; t >= 1; --t) {
+      const uint64_t r = below(draw(seed, kPurposeShuffle, epoch, (uint64_t)i, (uint64_t)t),
+                               (uint64_t)t + 1);
+      std::swap(perm[t], perm[r]);
+    }
+  }
+  e.seed = seed;
+  e.epoch = epoch;
+  e.n = n;
+  e.shard = shard;
+  e.valid = true;
+  return e.perm;
+}
+
+}  // namespace
+
 extern "C" nbsgd_status nbsgd_minibatch_indices(uint64_t seed, uint64_t step, int32_t n, int32_t m,
                                                 int32_t b, int32_t shard, int32_t* idx) {
   clear_error();
@@ -211,17 +248,10 @@ extern "C" nbsgd_status nbsgd_minibatch_indices(uint64_t seed, uint64_t step, in
   const int64_t per_epoch = shard / ((int64_t)m * b);
   const uint64_t epoch = step / (uint64_t)per_epoch;
   const int64_t window = (int64_t)(step % (uint64_t)per_epoch);
-  std::vector<int32_t> perm(shard);
-  for (int32_t i = 0; i < n; ++i) {
-    for (int32_t t = 0; t < shard; ++t) perm[t] = t;
-    for (int32_t t = shard - 1; t >= 1; --t) {
-      const uint64_t r = below(draw(seed, kPurposeShuffle, epoch, (uint64_t)i, (uint64_t)t),
-                               (uint64_t)t + 1);
-      std::swap(perm[t], perm[r]);
-    }
-    const int64_t base = window * m * b;
+  const std::vector<int32_t>& perm = epoch_permutations(seed, epoch, n, shard);
+  const int64_t base = window * m * b;
+  for (int32_t i = 0; i < n; ++i)
     for (int64_t k = 0; k < (int64_t)m * b; ++k)
-      idx[(int64_t)i * m * b + k] = (int32_t)((int64_t)shard * i + perm[base + k]);
-  }
+      idx[(int64_t)i * m * b + k] = (int32_t)((int64_t)shard * i + perm[(size_t)i * shard + base + k]);
   return NBSGD_OK;
 }

@@ -119,7 +119,10 @@ class MlpRunner:
             x0 = mlp_data.student_init(wl.seed, wl.d_in, wl.hidden, wl.classes)
         self.data = torch.from_numpy(np.ascontiguousarray(data, dtype=np.float32)).to(dev)
         self.labels = torch.from_numpy(np.ascontiguousarray(labels, dtype=np.int32)).to(dev)
-        self.X = torch.from_numpy(np.ascontiguousarray(x0, dtype=np.float32)).to(dev).repeat(wl.n, 1)
+        x0 = np.asarray(x0, dtype=np.float32)
+        row = np.zeros(self.P, np.float32)  # the library's layout pads the vector with zeros
+        row[:x0.size] = x0
+        self.X = torch.from_numpy(row).to(dev).repeat(wl.n, 1)
         self.V = torch.zeros_like(self.X)
         self.G = torch.zeros((wl.n, wl.m, self.P), dtype=torch.float32, device=dev)
         self.losses = torch.zeros(wl.n * wl.m, dtype=torch.float32, device=dev)

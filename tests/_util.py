@@ -94,6 +94,15 @@ def mlp_blocks(d_in, hidden, classes):
     return [("W1", 0, b1), ("b1", b1, w2), ("W2", w2, b2), ("b2", b2, b2 + classes)]
 
 
+def pad_cols(X, P):
+    """X with zero columns appended up to P (the library pads the flat MLP
+    vector to a multiple of 4 floats; the oracle's vector is unpadded)."""
+    X = np.asarray(X)
+    out = np.zeros(X.shape[:-1] + (P,), X.dtype)
+    out[..., :X.shape[-1]] = X
+    return out
+
+
 def rel_err_blocks(got, want, blocks) -> float:
     """Largest per-block rel_err along the last axis: each parameter block is
     measured against its own rms, so blocks of very different scale (1.57M

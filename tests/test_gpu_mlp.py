@@ -13,7 +13,7 @@ import oracle
 from oracle.mlp import BF16, Shape
 from paper_2211_00889_amd import _lib, runner
 from synth import mlp_data, workloads
-from tests._util import mlp_blocks, rel_err_blocks
+from tests._util import mlp_blocks, pad_cols, rel_err_blocks
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -50,7 +50,7 @@ def test_grad_small_shape_every_entry(tiny):
     idx = rng.integers(0, wl.n_samples, size=(wl.n, wl.m, wl.batch)).astype(np.int32)
     _say(f"mlp grad small n={wl.n} m={wl.m} finished={int(mask.sum())}")
     r = runner.MlpRunner(wl, DEV, A, y, x0)
-    Xd = torch.from_numpy(X).to(DEV)
+    Xd = torch.from_numpy(pad_cols(X, r.P)).to(DEV)
     r.G.fill_(7.0)
     r.losses.fill_(-1.0)
     _lib.mlp_grad(Xd, wl.m, r.dims, r.data, r.labels, idx, mask, r.G, r.losses, r.workspace)
@@ -62,6 +62,7 @@ def test_grad_small_shape_every_entry(tiny):
             if mask[i, j]:
                 g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
                 assert rel_err_blocks(G[i, j], g, mlp_blocks(*r.dims)) <= TOL_BF16, (i, j)
+                assert (G[i, j, s.n_params:] == 0).all()  # the padding
                 assert abs(L[i, j] - loss) <= TOL_BF16 * abs(loss)
             else:
                 assert (G[i, j] == 7.0).all() and L[i, j] == -1.0
@@ -112,7 +113,7 @@ def test_eval_loss_of_average_replica(tiny):
     r = runner.MlpRunner(wl, DEV, A, y, x0)
     rng = np.random.default_rng(1)
     X = (x0[None, :] + 0.1 * rng.standard_normal((wl.n, s.n_params))).astype(np.float32)
-    r.X.copy_(torch.from_numpy(X))
+    r.X.copy_(torch.from_numpy(pad_cols(X, r.P)))
     _say("mlp eval of the average replica")
     got = r.evaluate().cpu().numpy()
     ev = wl.eval_indices()

@@ -178,7 +178,9 @@ def test_minibatch_indices_errors():
 
 
 def test_mlp_shape_checks():
-    assert nb._lib.mlp_param_count(3072, 512, 10) == 1_578_506
+    assert nb._lib.mlp_param_count(3072, 512, 10) == 1_578_508  # 1,578,506 padded to 4
+    assert nb._lib.mlp_param_count(128, 64, 10) == 8908  # 8,906 padded
+    assert nb._lib.mlp_param_count(128, 64, 12) == 9036  # 9,036: no padding
     for bad in ((3000, 512, 10), (3072, 520, 10), (3072, 1024, 10), (3072, 512, 17), (3072, 512, 1)):
         with pytest.raises(nb.NbsgdError) as e:
             nb._lib.mlp_param_count(*bad)
