@@ -192,3 +192,49 @@ def test_blocking_baseline_small_shape_matches_oracle(tiny):
     # the non-blocking schedule of the same iterations is never slower
     nb_secs = [runner.Schedule(wl).mask(k)[3][2] for k in range(wl.steps)]
     assert all(a <= b for a, b in zip(nb_secs, secs))
+
+
+def test_grad_two_launch_groups_and_wide_indices():
+    """1,024 mini-batches (16 learners x 64), more than one launch's list, on
+    a data set of 70,000 samples (indices above 65,535 travel as 32-bit
+    words).  Sampled entries around the group boundary and at both ends."""
+    wl = dataclasses.replace(workloads.MLP_TINY, n=16, m=64, n_samples=70_000)
+    s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
+    A, y, x0 = _data(wl)
+    rng = np.random.default_rng(5)
+    X = (x0[None, :] + 0.05 * rng.standard_normal((wl.n, s.n_params))).astype(np.float32)
+    mask = np.ones((wl.n, wl.m), np.uint8)
+    mask[3, 10:] = 0
+    mask[15, 1:] = 0
+    idx = rng.integers(0, wl.n_samples, size=(wl.n, wl.m, wl.batch)).astype(np.int32)
+    idx[0, 0, :] = wl.n_samples - 1 - np.arange(wl.batch)  # the largest indices
+    _say(f"mlp grad n={wl.n} m={wl.m} finished={int(mask.sum())} n_samples={wl.n_samples}")
+    r = runner.MlpRunner(wl, DEV, A, y, x0)
+    Xd = torch.from_numpy(pad_cols(X, r.P)).to(DEV)
+    r.G.fill_(7.0)
+    _lib.mlp_grad(Xd, wl.m, r.dims, r.data, r.labels, idx, mask, r.G, r.losses, r.workspace)
+    torch.cuda.synchronize()
+    L = r.losses.cpu().numpy().reshape(wl.n, wl.m)
+    finished = list(zip(*np.nonzero(mask)))
+    picks = [0, 1, 894, 895, 896, 897, len(finished) - 1]
+    for k in picks:
+        i, j = finished[k]
+        g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
+        assert rel_err_blocks(r.G[i, j].cpu().numpy(), g, mlp_blocks(*r.dims)) <= TOL_BF16, (k, i, j)
+        assert abs(L[i, j] - loss) <= TOL_BF16 * abs(loss)
+    assert (r.G[3, 10:] == 7.0).all() and (r.G[15, 1:] == 7.0).all()
+
+
+def test_loss_odd_batch_count(tiny):
+    """Three batches: the forward pairs two of them in one tile and leaves
+    the third alone."""
+    wl, A, y, x0 = tiny
+    s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
+    r = runner.MlpRunner(wl, DEV, A, y, x0)
+    idx = np.random.default_rng(2).integers(0, wl.n_samples, size=3 * 32).astype(np.int32)
+    out = torch.zeros(3, dtype=torch.float32, device=DEV)
+    _say("mlp loss, 3 batches")
+    _lib.mlp_loss(r.X[1], r.dims, r.data, r.labels, idx, out, r.workspace)
+    got = out.cpu().numpy()
+    want = [oracle.mlp.forward(x0, A[idx[k:k + 32]], y[idx[k:k + 32]], s, BF16)[0] for k in (0, 32, 64)]
+    np.testing.assert_allclose(got, want, rtol=TOL_BF16)
