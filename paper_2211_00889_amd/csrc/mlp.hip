@@ -72,7 +72,7 @@ struct IdxChunk {
 // kernel arguments are limited to 4 KiB: the list, the shapes, the forward
 // map and at most ten pointers or 64-bit scalars
 static_assert(sizeof(List) + sizeof(Dims) + 180 + 10 * 8 <= 4096, "kernel arguments exceed 4 KiB");
-static_assert(sizeof(IdxChunk) + 16 <= 4096, "kernel arguments exceed 4 KiB");
+static_assert(sizeof(IdxChunk) + 32 <= 4096, "kernel arguments exceed 4 KiB");
 static_assert(kMaxList <= 4096 && kMaxEval <= 4096, "slots are packed in 16 bits");
 
 __device__ __forceinline__ int item_learner(uint32_t w) { return (int)(w >> 24); }
@@ -89,13 +89,19 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return (uint32_t)ua | ((uint32_t)ub << 16);
 }
 
-__global__ void __launch_bounds__(256) k_put_idx(int32_t* __restrict__ dst, IdxChunk c) {
+// Writes the sample index and its label (clamped into [0, classes)) of every
+// row of the listed mini-batches.
+__global__ void __launch_bounds__(256)
+    k_put_idx(int32_t* __restrict__ dst, int32_t* __restrict__ ylab,
+              const int32_t* __restrict__ labels, int32_t classes, IdxChunk c) {
   const int t = blockIdx.x * 256 + threadIdx.x;
   const int k = t >> 5, r = t & 31;
   if (k >= c.n_slots) return;
   const int slot = (int)((c.slot[k >> 1] >> (16 * (k & 1))) & 0xffffu);
   const int32_t v = c.wide ? (int32_t)c.v[t] : (int32_t)((c.v[t >> 1] >> (16 * (t & 1))) & 0xffffu);
+  const int32_t y = labels[v];
   dst[slot * kBatch + r] = v;
+  ylab[slot * kBatch + r] = y < 0 ? 0 : (y >= classes ? classes - 1 : y);
 }
 
 // Forward work items: the (tile, 64-unit block) pairs in order learner,
@@ -273,20 +279,22 @@ __global__ void __launch_bounds__(512)
 // (shares summed in unit-block order, + b2), softmax cross-entropy and dZ2 =
 // (softmax - onehot) / 32 (recomputed by every unit block: 32 x classes
 // values).  Unit block 0 writes the loss and, when BACKWARD, db2 and the
-// padding of G.  When BACKWARD, each block writes dW2 and db1 of its units,
-// and dZ1 of its units in bf16 as [slot][unit][row] for k_mlp_wgrad.
+// padding of G.  When BACKWARD, wave w takes the 16 units c0 + 16w .. on
+// the matrix cores: dZ1 = (bf16(dZ2) bf16(W2)^T) * [Z1 > 0] (K = classes,
+// zero-padded to 32), stored in bf16 as [slot][unit][row] for k_mlp_wgrad,
+// db1 = its sum over the rows, and dW2 = bf16(relu(Z1))^T bf16(dZ2) (K = the
+// 32 rows).
 template <bool BACKWARD>
 __global__ void __launch_bounds__(256)
-    k_mlp_head(const float* __restrict__ X, const int32_t* __restrict__ labels,
-               const int32_t* __restrict__ idx, const float* __restrict__ Z1,
-               const float* __restrict__ Zp, int64_t zp_stride, __bf16* __restrict__ dZ1t,
-               float* __restrict__ G, float* __restrict__ losses, Dims d, List L) {
+    k_mlp_head(const float* __restrict__ X, const int32_t* __restrict__ ylab,
+               const float* __restrict__ Z1, const float* __restrict__ Zp, int64_t zp_stride,
+               __bf16* __restrict__ dZ1t, float* __restrict__ G, float* __restrict__ losses, Dims d,
+               List L) {
   constexpr int kLdz = 64 + 1;
   __shared__ float Zs[kBatch * kMaxClasses];  // logits, then dZ2
-  __shared__ float Zb[kBatch * kMaxClasses];  // bf16(dZ2)
+  __shared__ float Zb[kBatch * kMaxClasses];  // bf16(dZ2), zero beyond the classes
   __shared__ float W2s[64 * kMaxClasses];     // bf16(W2) of this block's units
   __shared__ float Z1s[kBatch * kLdz];        // Z1 of this block's units
-  __shared__ float dZs[kBatch * kLdz];        // dZ1 of this block's units
   __shared__ float row_loss[kBatch];
   __shared__ int ys[kBatch];
   const uint32_t item = L.w[blockIdx.x];
@@ -295,23 +303,22 @@ __global__ void __launch_bounds__(256)
   const int H = d.hidden, C = d.classes;
   const int blocks = H / 64;
   const int c0 = blockIdx.y * 64;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t row0 = (int64_t)slot * kBatch;
 
+  // every load of this phase is independent of the others
   for (int o = tid; o < kBatch * C; o += 256) {
     const int r = o / C, c = o % C;
     float z = 0.0f;
     for (int q = 0; q < blocks; ++q) z += Zp[(int64_t)q * zp_stride + (row0 + r) * kMaxClasses + c];
     Zs[r * kMaxClasses + c] = z + prm[d.off_b2 + c];
   }
-  if (tid < kBatch) {
-    const int y = labels[idx[row0 + tid]];
-    ys[tid] = y < 0 ? 0 : (y >= C ? C - 1 : y);
-  }
+  if (tid < kBatch) ys[tid] = ylab[row0 + tid];
   if (BACKWARD) {
     for (int k = tid; k < 64 * C; k += 256) W2s[k] = bf16r(prm[d.off_w2 + (int64_t)c0 * C + k]);
-    for (int o = tid; o < kBatch * 64; o += 256) {
-      const int r = o >> 6, h = o & 63;
+#pragma unroll
+    for (int u = 0; u < kBatch * 64 / 256; ++u) {
+      const int o = tid + 256 * u, r = o >> 6, h = o & 63;
       Z1s[r * kLdz + h] = Z1[(row0 + r) * H + c0 + h];
     }
   }
@@ -326,8 +333,8 @@ __global__ void __launch_bounds__(256)
     const float lse = zmax + logf(sum);
     row_loss[r] = lse - z[ys[r]];
     if (BACKWARD)
-      for (int c = 0; c < C; ++c) {
-        const float g = (expf(z[c] - lse) - (c == ys[r] ? 1.0f : 0.0f)) * (1.0f / kBatch);
+      for (int c = 0; c < kMaxClasses; ++c) {
+        const float g = c < C ? (expf(z[c] - lse) - (c == ys[r] ? 1.0f : 0.0f)) * (1.0f / kBatch) : 0.0f;
         Zs[r * kMaxClasses + c] = g;
         Zb[r * kMaxClasses + c] = bf16r(g);
       }
@@ -350,25 +357,53 @@ __global__ void __launch_bounds__(256)
     }
   }
   if (!BACKWARD) return;
-  for (int o = tid; o < 64 * C; o += 256) {  // dW2[c0 + h][c]
-    const int h = o / C, c = o % C;
-    float s = 0.0f;
-    for (int r = 0; r < kBatch; ++r) s += bf16r(fmaxf(Z1s[r * kLdz + h], 0.0f)) * Zb[r * kMaxClasses + c];
-    g[d.off_w2 + (int64_t)c0 * C + o] = s;
+  const int hl = 16 * wave + (lane & 15);  // this lane's unit within the block
+  const int kq = 8 * (lane >> 4);          // this lane's K offset in a fragment
+  // dZ1 for rows 16 rt .. +15 and units 16w .. +15
+  bf16x8 fw;  // B[k][h] = bf16(W2[h][k]), k = class
+#pragma unroll
+  for (int t = 0; t < 8; ++t) fw[t] = (__bf16)(kq + t < C ? W2s[hl * C + kq + t] : 0.0f);
+  float db1 = 0.0f;
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt) {
+    bf16x8 fz;  // A[r][k] = bf16(dZ2[r][k])
+#pragma unroll
+    for (int t = 0; t < 8; ++t) fz[t] = (__bf16)(kq + t < kMaxClasses ? Zb[(16 * rt + (lane & 15)) * kMaxClasses + kq + t] : 0.0f);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fz, fw, acc, 0, 0, 0);
+    // lane holds rows 16 rt + 4 (lane / 16) + t of unit hl
+    const int r0 = 16 * rt + 4 * (lane >> 4);
+    float v[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      v[t] = Z1s[(r0 + t) * kLdz + hl] > 0.0f ? acc[t] : 0.0f;
+      db1 += v[t];
+    }
+    const uint2 packed = {pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+    *reinterpret_cast<uint2*>(dZ1t + ((int64_t)slot * H + c0 + hl) * kBatch + r0) = packed;
   }
-  for (int o = tid; o < kBatch * 64; o += 256) {  // dZ1[r][c0 + h], r fastest
-    const int h = o >> 5, r = o & 31;
-    float s = 0.0f;
-    for (int c = 0; c < C; ++c) s += Zb[r * kMaxClasses + c] * W2s[h * C + c];
-    const float v = Z1s[r * kLdz + h] > 0.0f ? s : 0.0f;
-    dZs[r * kLdz + h] = v;
-    dZ1t[((int64_t)slot * H + c0 + h) * kBatch + r] = (__bf16)v;
-  }
-  __syncthreads();
-  if (tid < 64) {
-    float s = 0.0f;
-    for (int r = 0; r < kBatch; ++r) s += dZs[r * kLdz + tid];
-    g[d.off_b1 + c0 + tid] = s;
+  // db1: the four row groups of a unit sit in lanes l, l+16, l+32, l+48
+  db1 += __shfl_xor(db1, 16);
+  db1 += __shfl_xor(db1, 32);
+  if (lane < 16) g[d.off_b1 + c0 + hl] = db1;
+  // dW2[h][c] for units 16w .. +15: A[h][r] = bf16(relu(Z1[r][h])), B[r][c] = bf16(dZ2[r][c])
+  {
+    bf16x8 fh, fd;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      fh[t] = (__bf16)fmaxf(Z1s[(kq + t) * kLdz + hl], 0.0f);
+      fd[t] = (__bf16)Zb[(kq + t) * kMaxClasses + (lane & 15)];
+    }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, fd, acc, 0, 0, 0);
+    const int c = lane & 15;
+    if (c < C) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int h = c0 + 16 * wave + 4 * (lane >> 4) + t;
+        g[d.off_w2 + (int64_t)h * C + c] = acc[t];
+      }
+    }
   }
 }
 
@@ -459,16 +494,17 @@ nbsgd_status check_shape(const nbsgd_mlp_shape* s, Dims* d) {
 
 size_t up256(size_t b) { return (b + 255) & ~(size_t)255; }
 
-// sample list, Z1 [rows][hidden] fp32, hidden/64 logit-share planes
+// sample list, labels, Z1 [rows][hidden] fp32, hidden/64 logit-share planes
 // [rows][16] fp32 and dZ1 [rows/32][hidden][32] bf16, each 256-byte aligned
 size_t workspace_for(const Dims& d, int64_t rows) {
-  return up256((size_t)rows * 4) + up256((size_t)rows * d.hidden * 4) +
+  return 2 * up256((size_t)rows * 4) + up256((size_t)rows * d.hidden * 4) +
          (size_t)(d.hidden / 64) * up256((size_t)rows * kMaxClasses * 4) +
          up256((size_t)rows * d.hidden * 2);
 }
 
 struct Workspace {
   int32_t* idx;
+  int32_t* ylab;
   float* z1;
   float* zp;
   int64_t zp_stride;  // floats between logit-share planes
@@ -479,6 +515,8 @@ Workspace carve(void* ws, const Dims& d, int64_t rows) {
   char* p = static_cast<char*>(ws);
   Workspace w;
   w.idx = reinterpret_cast<int32_t*>(p);
+  p += up256((size_t)rows * 4);
+  w.ylab = reinterpret_cast<int32_t*>(p);
   p += up256((size_t)rows * 4);
   w.z1 = reinterpret_cast<float*>(p);
   p += up256((size_t)rows * d.hidden * 4);
@@ -492,7 +530,7 @@ Workspace carve(void* ws, const Dims& d, int64_t rows) {
 // Copies the sample indices of the mini-batches `slots` (host idx[slot*32 ..])
 // to the workspace through kernel arguments, after checking every one.
 nbsgd_status upload_idx(const int32_t* host, const int32_t* slots, int n_slots, int64_t n_samples,
-                        int32_t* dst, hipStream_t s) {
+                        const int32_t* labels, const Dims& d, const Workspace& w, hipStream_t s) {
   for (int k = 0; k < n_slots; ++k)
     for (int r = 0; r < kBatch; ++r) {
       const int64_t pos = (int64_t)slots[k] * kBatch + r;
@@ -516,7 +554,8 @@ nbsgd_status upload_idx(const int32_t* host, const int32_t* slots, int n_slots, 
         else c.v[t >> 1] |= (uint32_t)src[r] << (16 * (t & 1));
       }
     }
-    hipLaunchKernelGGL(k_put_idx, dim3((c.n_slots * kBatch + 255) / 256), dim3(256), 0, s, dst, c);
+    hipLaunchKernelGGL(k_put_idx, dim3((c.n_slots * kBatch + 255) / 256), dim3(256), 0, s, w.idx,
+                       w.ylab, labels, d.classes, c);
   }
   return NBSGD_OK;
 }
@@ -536,8 +575,7 @@ uint32_t item(int learner, int slot_a, int slot_b) {
 // consecutive mini-batches of the same learner.
 template <bool BACKWARD>
 void launch_group(const std::pair<int, int>* mb, int count, const float* X, const float* data,
-                  const int32_t* labels, const Workspace& w, float* G, float* losses,
-                  const Dims& d, hipStream_t st) {
+                  const Workspace& w, float* G, float* losses, const Dims& d, hipStream_t st) {
   const int nb = d.hidden / 64;
   List tiles, items;
   FwdMap M;
@@ -568,7 +606,7 @@ void launch_group(const std::pair<int, int>* mb, int count, const float* X, cons
   hipLaunchKernelGGL(k_mlp_fwd, dim3(8 * per_xcd), dim3(512), 0, st, X, data, w.idx, w.z1, w.zp,
                      w.zp_stride, d, M, tiles);
   hipLaunchKernelGGL(k_mlp_head<BACKWARD>, dim3(items.count, BACKWARD ? nb : 1), dim3(256), 0, st, X,
-                     labels, w.idx, w.z1, w.zp, w.zp_stride, w.dz1t, G, losses, d, items);
+                     w.ylab, w.z1, w.zp, w.zp_stride, w.dz1t, G, losses, d, items);
   if (BACKWARD)
     hipLaunchKernelGGL(k_mlp_wgrad, dim3(items.count, d.d_in / kFeatBlock), dim3(256), 0, st, data,
                        w.idx, w.dz1t, G, d, items);
@@ -618,18 +656,18 @@ extern "C" nbsgd_status nbsgd_mlp_grad(const float* X, int32_t n, int32_t m, con
   std::vector<int32_t> finished;
   for (int32_t k = 0; k < n * m; ++k)
     if (mask[k]) finished.push_back(k);
-  if (nbsgd_status r = upload_idx(idx, finished.data(), (int)finished.size(), n_samples, w.idx, st))
+  if (nbsgd_status r = upload_idx(idx, finished.data(), (int)finished.size(), n_samples, labels, d, w, st))
     return r;
   std::pair<int, int> mb[kMaxList];
   int count = 0;
   for (int32_t k : finished) {
     mb[count++] = {k / m, k};
     if (count == kMaxList) {
-      launch_group<true>(mb, count, X, data, labels, w, G, losses, d, st);
+      launch_group<true>(mb, count, X, data, w, G, losses, d, st);
       count = 0;
     }
   }
-  if (count) launch_group<true>(mb, count, X, data, labels, w, G, losses, d, st);
+  if (count) launch_group<true>(mb, count, X, data, w, G, losses, d, st);
   return launch_err("nbsgd_mlp_grad");
 }
 
@@ -659,7 +697,7 @@ extern "C" nbsgd_status nbsgd_mlp_loss(const float* params, const nbsgd_mlp_shap
     mb[k] = {0, k};
     slots[k] = k;
   }
-  if (nbsgd_status r = upload_idx(idx, slots, count / kBatch, n_samples, w.idx, st)) return r;
-  launch_group<false>(mb, count / kBatch, params, data, labels, w, nullptr, losses, d, st);
+  if (nbsgd_status r = upload_idx(idx, slots, count / kBatch, n_samples, labels, d, w, st)) return r;
+  launch_group<false>(mb, count / kBatch, params, data, w, nullptr, losses, d, st);
   return launch_err("nbsgd_mlp_loss");
 }
