@@ -191,6 +191,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded SplitMix64 Irwin-Hall normals: X ~ N(0, 1), G ~ N(0, 1e-3))",
         "config": {"workload": wl.name, "n_learners": wl.n, "minibatches": wl.m, "P": wl.P,
+                   "row_stride": r.ld,
                    "mixing": wl.mixing, "order": wl.order, "delay": wl.delay.kind,
                    "lr": wl.lr, "momentum": wl.momentum,
                    "mean_finished_per_step": float(np.mean(sum_counts))},

@@ -174,6 +174,27 @@ nbsgd_status nbsgd_step(float *X, float *V, const float *G, const uint8_t *mask,
                         int32_t n, int32_t m, int64_t P, float lr, float momentum, int32_t order,
                         void *stream);
 
+/* nbsgd_step on rows `ld` floats apart: row i of X and V starts at X + i*ld,
+ * V + i*ld, and row (i, j) of G at G + (i*m + j)*ld; only the first P floats
+ * of a row are read or written (the rest of each row is never touched).
+ * ld >= P (NBSGD_E_SHAPE).  The vector width is the largest of 4, 2, 1
+ * dividing both P and ld.  nbsgd_step is this call with ld = P.
+ * Errors: as nbsgd_step.                                                    */
+nbsgd_status nbsgd_step_strided(float *X, float *V, const float *G, int64_t ld,
+                                const uint8_t *mask, const float *W, int32_t n, int32_t m,
+                                int64_t P, float lr, float momentum, int32_t order, void *stream);
+
+/* Row stride (in floats) to allocate X, V and G with for nbsgd_step_strided:
+ * P when P < 2^22, else k * 2^22 with k = ceil(P / 2^22), or the next
+ * integer that is not a power of two when k is one (k = 1 gives 3), so every
+ * row starts on a 16 MiB boundary without a power-of-two stride.  Measured on
+ * MI355X for the fused step: the HBM throughput depends on where the rows
+ * start relative to each other (the DRAM address mapping); this stride raised
+ * the sustained rate of the 11.2M-, 23.5M- and 138M-parameter workloads by
+ * 3-6% (k = 3, 6, 33), whereas a power-of-two stride lowered it by up to 8%.
+ * Errors: NBSGD_E_ARG (null ld), NBSGD_E_SHAPE (P < 0).                    */
+nbsgd_status nbsgd_row_stride(int64_t P, int64_t *ld);
+
 /* ------------------------------------------------------- mixing matrices
  * Host builders, W fp32 [n*n] row-major, caller-owned.
  * nbsgd_w_allreduce: every entry 1/n (ring all-reduce averages all replicas,

@@ -24,6 +24,7 @@ MAX_LEARNERS, MAX_MINIBATCHES = 16, 64
 SLOW_NONE, SLOW_RANDOM = -1, -2
 
 EXPORTS = ("nbsgd_sample_mask", "nbsgd_accumulate", "nbsgd_mix", "nbsgd_update", "nbsgd_step",
+           "nbsgd_step_strided", "nbsgd_row_stride",
            "nbsgd_w_allreduce", "nbsgd_w_ring", "nbsgd_matcha_create", "nbsgd_matcha_w",
            "nbsgd_matcha_matchings", "nbsgd_matcha_set", "nbsgd_matcha_get", "nbsgd_matcha_optimize",
            "nbsgd_matcha_destroy", "nbsgd_mlp_param_count",
@@ -69,6 +70,9 @@ def load():
                          _c_void_p],
         "nbsgd_step": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i64,
                        _f32, _f32, _i32, _c_void_p],
+        "nbsgd_step_strided": [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p, _i32, _i32,
+                               _i64, _f32, _f32, _i32, _c_void_p],
+        "nbsgd_row_stride": [_i64, ctypes.POINTER(_i64)],
         "nbsgd_w_allreduce": [_i32, _c_void_p],
         "nbsgd_w_ring": [_i32, _c_void_p],
         "nbsgd_matcha_create": [_u64, _i32, _i32, ctypes.POINTER(_c_void_p)],
@@ -254,6 +258,24 @@ def step(X, V, G, mask, W, lr: float, momentum: float, order: int, stream=None):
     W = _w32(W, n)
     _check(load().nbsgd_step(_dev(X, "X"), _dev(V, "V"), _dev(G, "G"), _host_ptr(mask),
                              _host_ptr(W), n, m, P, lr, momentum, order, _stream(X, stream)))
+
+
+def step_strided(X, V, G, P: int, mask, W, lr: float, momentum: float, order: int, stream=None):
+    """nbsgd_step on padded rows: X, V [n, ld], G [n, m, ld]; the first P
+    columns of each row are the parameters."""
+    n, m, ld = G.shape
+    if tuple(X.shape) != (n, ld) or tuple(V.shape) != (n, ld):
+        raise ValueError("X and V must be [n, ld] with G [n, m, ld]")
+    mask = _u8(mask, (n, m))
+    W = _w32(W, n)
+    _check(load().nbsgd_step_strided(_dev(X, "X"), _dev(V, "V"), _dev(G, "G"), ld, _host_ptr(mask),
+                                     _host_ptr(W), n, m, P, lr, momentum, order, _stream(X, stream)))
+
+
+def row_stride(P: int) -> int:
+    ld = _i64(0)
+    _check(load().nbsgd_row_stride(P, ctypes.byref(ld)))
+    return ld.value
 
 
 # ------------------------------------------------------------ MLP workload

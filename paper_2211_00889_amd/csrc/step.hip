@@ -32,6 +32,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
+
 #include "internal.h"
 
 using namespace nbsgd;
@@ -186,7 +188,7 @@ __device__ __forceinline__ typename Vec<VEC>::type mix_all(const typename Vec<VE
 template <int VEC, int ORDER>
 __global__ void __launch_bounds__(kStepBlock)
     k_step(float* __restrict__ Xf, float* __restrict__ Vf, const float* __restrict__ Gf,
-           int64_t pv, int n, float mu, StepPlan S, Mixing W) {
+           int64_t pv, int64_t ldv, int n, float mu, StepPlan S, Mixing W) {
   using vf = typename Vec<VEC>::type;
   extern __shared__ char smem[];
   vf* zs = reinterpret_cast<vf*>(smem);        // [n][64]: values to be mixed
@@ -208,8 +210,8 @@ __global__ void __launch_bounds__(kStepBlock)
     xo[s] = (vf)(0.0f);
     vo[s] = (vf)(0.0f);
     if (p < n && live) {
-      xo[s] = ld_stream(X + (int64_t)p * pv + v);
-      vo[s] = ld_stream(V + (int64_t)p * pv + v);
+      xo[s] = ld_stream(X + (int64_t)p * ldv + v);
+      vo[s] = ld_stream(V + (int64_t)p * ldv + v);
     }
   }
   const int e_end = S.seg[wave + 1];
@@ -223,7 +225,7 @@ __global__ void __launch_bounds__(kStepBlock)
 #pragma unroll
     for (int k = 0; k < kChunk; ++k) {
       const int64_t row = (e + k < e_end) ? (int64_t)half_of(S.row, e + k) : 0;  // uniform
-      a[k] = (e + k < e_end && live) ? ld_stream(G + row * pv + v) : (vf)(0.0f);
+      a[k] = (e + k < e_end && live) ? ld_stream(G + row * ldv + v) : (vf)(0.0f);
     }
 #pragma unroll
     for (int k = 0; k < kChunk; ++k) {
@@ -253,7 +255,7 @@ __global__ void __launch_bounds__(kStepBlock)
       vf g = (vf)(0.0f);
       for (int r = S.lslot[q]; r < S.lslot[q + 1]; ++r) g += part[r * kWave + lane];
       const vf vn = mu * vo[s] + g * S.inv_c[q];
-      if (live) st_stream(V + (int64_t)q * pv + v, vn);
+      if (live) st_stream(V + (int64_t)q * ldv + v, vn);
       if (ORDER == NBSGD_MIX_THEN_STEP) {
         zs[q * kWave + lane] = xo[s];
         keep[s] = S.eta[q] * vn;
@@ -273,7 +275,7 @@ __global__ void __launch_bounds__(kStepBlock)
     if (i < n && live) {
       vf x = W.uniform ? total : mix_row<VEC>(zs, kWave, W, i, lane);
       if (ORDER == NBSGD_MIX_THEN_STEP) x -= keep[s];
-      st_stream(X + (int64_t)i * pv + v, x);
+      st_stream(X + (int64_t)i * ldv + v, x);
     }
   }
 }
@@ -435,22 +437,25 @@ nbsgd_status plan_from_mask(const uint8_t* mask, int32_t n, int32_t m, float lr,
 }
 
 template <int VEC, int ORDER>
-void launch_step(float* X, float* V, const float* G, int64_t pv, int n, float mu,
+void launch_step(float* X, float* V, const float* G, int64_t pv, int64_t ldv, int n, float mu,
                  const StepPlan& S, int runs, const Mixing& W, hipStream_t s) {
   const int64_t blocks = (pv + kWave - 1) / kWave;
   const size_t lds = (size_t)(n + runs) * kWave * VEC * sizeof(float);
   hipLaunchKernelGGL((k_step<VEC, ORDER>), dim3((unsigned)blocks), dim3(kStepBlock), lds, s, X,
-                     V, G, pv, n, mu, S, W);
+                     V, G, pv, ldv, n, mu, S, W);
 }
 
-}  // namespace
+// Rows of 2^22 floats (16 MiB) or more start on 16 MiB boundaries when the
+// stride is a multiple of 2^22 floats (see nbsgd_row_stride).
+constexpr int64_t kRowAlign = int64_t(1) << 22;
 
-extern "C" nbsgd_status nbsgd_step(float* X, float* V, const float* G, const uint8_t* mask,
-                                   const float* Wh, int32_t n, int32_t m, int64_t P, float lr,
-                                   float momentum, int32_t order, void* stream) {
-  clear_error();
+// The fused step on rows `ld` floats apart (ld >= P).
+nbsgd_status step_impl(float* X, float* V, const float* G, int64_t ld, const uint8_t* mask,
+                       const float* Wh, int32_t n, int32_t m, int64_t P, float lr, float momentum,
+                       int32_t order, void* stream) {
   if (nbsgd_status st = check_nm(n, m)) return st;
   if (P < 0) return fail(NBSGD_E_SHAPE, "P=%lld is negative", (long long)P);
+  if (ld < P) return fail(NBSGD_E_SHAPE, "row stride %lld is below P=%lld", (long long)ld, (long long)P);
   if (order != NBSGD_MIX_THEN_STEP && order != NBSGD_STEP_THEN_MIX)
     return fail(NBSGD_E_ARG, "unknown order %d", order);
   StepPlan S;
@@ -462,25 +467,57 @@ extern "C" nbsgd_status nbsgd_step(float* X, float* V, const float* G, const uin
   if (nbsgd_status st = check_rows(X, "X")) return st;
   if (nbsgd_status st = check_rows(V, "V")) return st;
   if (nbsgd_status st = check_rows(G, "G")) return st;
-  const int64_t xb = (int64_t)n * P * 4, gb = (int64_t)n * m * P * 4;
+  // extents: the last row needs only P floats
+  const int64_t xb = ((int64_t)(n - 1) * ld + P) * 4, gb = ((int64_t)n * m - 1) * ld * 4 + P * 4;
   if (overlap(X, xb, V, xb)) return fail(NBSGD_E_ARG, "X and V overlap");
   if (overlap(G, gb, X, xb) || overlap(G, gb, V, xb))
     return fail(NBSGD_E_ARG, "G overlaps X or V");
-  const int vec = vec_width(P);
-  const int64_t pv = P / vec;
+  const int vec = std::min(vec_width(P), vec_width(ld));  // divides both P and ld
+  const int64_t pv = P / vec, ldv = ld / vec;
   if ((pv + kWave - 1) / kWave > 0x7fffffff)
     return fail(NBSGD_E_UNSUPPORTED, "P=%lld needs too many workgroups", (long long)P);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (order == NBSGD_MIX_THEN_STEP) {
-    if (vec == 4) launch_step<4, NBSGD_MIX_THEN_STEP>(X, V, G, pv, n, momentum, S, runs, W, s);
-    else if (vec == 2) launch_step<2, NBSGD_MIX_THEN_STEP>(X, V, G, pv, n, momentum, S, runs, W, s);
-    else launch_step<1, NBSGD_MIX_THEN_STEP>(X, V, G, pv, n, momentum, S, runs, W, s);
+    if (vec == 4) launch_step<4, NBSGD_MIX_THEN_STEP>(X, V, G, pv, ldv, n, momentum, S, runs, W, s);
+    else if (vec == 2) launch_step<2, NBSGD_MIX_THEN_STEP>(X, V, G, pv, ldv, n, momentum, S, runs, W, s);
+    else launch_step<1, NBSGD_MIX_THEN_STEP>(X, V, G, pv, ldv, n, momentum, S, runs, W, s);
   } else {
-    if (vec == 4) launch_step<4, NBSGD_STEP_THEN_MIX>(X, V, G, pv, n, momentum, S, runs, W, s);
-    else if (vec == 2) launch_step<2, NBSGD_STEP_THEN_MIX>(X, V, G, pv, n, momentum, S, runs, W, s);
-    else launch_step<1, NBSGD_STEP_THEN_MIX>(X, V, G, pv, n, momentum, S, runs, W, s);
+    if (vec == 4) launch_step<4, NBSGD_STEP_THEN_MIX>(X, V, G, pv, ldv, n, momentum, S, runs, W, s);
+    else if (vec == 2) launch_step<2, NBSGD_STEP_THEN_MIX>(X, V, G, pv, ldv, n, momentum, S, runs, W, s);
+    else launch_step<1, NBSGD_STEP_THEN_MIX>(X, V, G, pv, ldv, n, momentum, S, runs, W, s);
   }
   return check_launch("nbsgd_step");
+}
+
+}  // namespace
+
+extern "C" nbsgd_status nbsgd_step(float* X, float* V, const float* G, const uint8_t* mask,
+                                   const float* Wh, int32_t n, int32_t m, int64_t P, float lr,
+                                   float momentum, int32_t order, void* stream) {
+  clear_error();
+  return step_impl(X, V, G, P, mask, Wh, n, m, P, lr, momentum, order, stream);
+}
+
+extern "C" nbsgd_status nbsgd_step_strided(float* X, float* V, const float* G, int64_t ld,
+                                           const uint8_t* mask, const float* Wh, int32_t n,
+                                           int32_t m, int64_t P, float lr, float momentum,
+                                           int32_t order, void* stream) {
+  clear_error();
+  return step_impl(X, V, G, ld, mask, Wh, n, m, P, lr, momentum, order, stream);
+}
+
+extern "C" nbsgd_status nbsgd_row_stride(int64_t P, int64_t* ld) {
+  clear_error();
+  if (!ld) return fail(NBSGD_E_ARG, "ld is null");
+  if (P < 0) return fail(NBSGD_E_SHAPE, "P=%lld is negative", (long long)P);
+  if (P < kRowAlign) {
+    *ld = P;
+    return NBSGD_OK;
+  }
+  int64_t k = (P + kRowAlign - 1) / kRowAlign;  // rows of k * 2^22 floats
+  if ((k & (k - 1)) == 0) k = k == 1 ? 3 : k + 1;  // a power-of-two stride aliases
+  *ld = k * kRowAlign;
+  return NBSGD_OK;
 }
 
 extern "C" nbsgd_status nbsgd_accumulate(const float* G, const uint8_t* mask, int32_t n, int32_t m,

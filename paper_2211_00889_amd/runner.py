@@ -56,7 +56,13 @@ class Schedule:
 
 
 class StepRunner:
-    """Replicas X, momentum V and gradients G of one workload on a device."""
+    """Replicas X, momentum V and gradients G of one workload on a device.
+
+    Rows are allocated ``ld = nbsgd_row_stride(P)`` floats apart (P itself
+    below 2^22, else a multiple of 2^22 so rows start on 16 MiB boundaries);
+    ``X``, ``V`` and ``G`` are the [.., P] views of the parameters.  Every row
+    holds the values the generator gives the contiguous [n, P] / [n, m, P]
+    tensor (flat index row * P + column)."""
 
     def __init__(self, wl, device="cuda:0", P: int | None = None, fill: bool = True):
         import torch
@@ -67,13 +73,19 @@ class StepRunner:
         self.wl = wl
         self.P = wl.P if P is None else P
         n, m, P = wl.n, wl.m, self.P
+        self.ld = _lib.row_stride(P)
         self.device = torch.device(device)
-        self.X = torch.empty((n, P), dtype=torch.float32, device=self.device)
-        self.V = torch.zeros((n, P), dtype=torch.float32, device=self.device)
-        self.G = torch.empty((n, m, P), dtype=torch.float32, device=self.device)
+        self.Xrows = torch.empty((n, self.ld), dtype=torch.float32, device=self.device)
+        self.Vrows = torch.zeros((n, self.ld), dtype=torch.float32, device=self.device)
+        self.Grows = torch.empty((n, m, self.ld), dtype=torch.float32, device=self.device)
+        self.X, self.V, self.G = self.Xrows[:, :P], self.Vrows[:, :P], self.Grows[:, :, :P]
         if fill:
-            synth_device.fill_normal(self.X, wl.seed, workloads.STREAM_X, wl.x_std)
-            synth_device.fill_normal(self.G, wl.seed, workloads.STREAM_G, wl.g_std)
+            for i in range(n):
+                synth_device.fill_normal(self.Xrows[i, :P], wl.seed, workloads.STREAM_X, wl.x_std,
+                                         first=i * P)
+                for j in range(m):
+                    synth_device.fill_normal(self.Grows[i, j, :P], wl.seed, workloads.STREAM_G,
+                                             wl.g_std, first=(i * m + j) * P)
         self.order = _ORDER[wl.order]
         self.mixer = Mixer(wl.mixing, n, wl.seed, wl.matcha_degree, wl.matcha_budget)
         self.schedule = Schedule(wl)
@@ -84,7 +96,8 @@ class StepRunner:
         return mask, counts, timing, self.mixer.w(step)
 
     def launch(self, mask, W, stream=None):
-        _lib.step(self.X, self.V, self.G, mask, W, self.wl.lr, self.wl.momentum, self.order, stream)
+        _lib.step_strided(self.Xrows, self.Vrows, self.Grows, self.P, mask, W, self.wl.lr,
+                          self.wl.momentum, self.order, stream)
 
     def run(self, steps: int, first: int = 0, stream=None):
         """Runs iterations first .. first+steps-1; returns the per-step counts."""

@@ -94,6 +94,49 @@ def test_step_matches_oracle(n, m, P, order):
         assert np.array_equal(Gd.cpu().numpy(), G)  # G is read-only
 
 
+STRIDED = [  # n, m, P, ld: the vector width is the largest of 4/2/1 dividing P and ld
+    (4, 4, 1030, 1036), (3, 5, 257, 300), (8, 8, 20000, 20004), (16, 4, 1024, 1280), (2, 3, 6, 7),
+    (5, 2, 1032, 1033),
+]
+
+
+@pytest.mark.parametrize("order", [nb.MIX_THEN_STEP, nb.STEP_THEN_MIX])
+@pytest.mark.parametrize("n,m,P,ld", STRIDED)
+def test_strided_step_matches_oracle_and_leaves_padding(n, m, P, ld, order):
+    rng = np.random.default_rng(n * 100 + P + ld + order)
+    X, V, G = _inputs(rng, n, m, P)
+    mask, W = _random_mask(rng, n, m), _birkhoff_w(rng, n)
+    pad = np.float32(12345.0)
+    Xp = np.full((n, ld), pad, np.float32)
+    Vp = np.full((n, ld), pad, np.float32)
+    Gp = np.full((n, m, ld), pad, np.float32)
+    Xp[:, :P], Vp[:, :P], Gp[:, :, :P] = X, V, G
+    _say(f"strided step n={n} m={m} P={P} ld={ld} order={order}")
+    Xd, Vd, Gd = _dev(Xp), _dev(Vp), _dev(Gp)
+    _lib.step_strided(Xd, Vd, Gd, P, mask, W, 0.1, 0.9, order)
+    Xc, Vc, Gc = _dev(X), _dev(V), _dev(G)
+    nb.step(Xc, Vc, Gc, mask, W, 0.1, 0.9, order)
+    torch.cuda.synchronize()
+    Xs, Vs = Xd.cpu().numpy(), Vd.cpu().numpy()
+    # the padding is never touched, and the columns equal the contiguous call bit for bit
+    assert (Xs[:, P:] == pad).all() and (Vs[:, P:] == pad).all()
+    assert np.array_equal(Gd.cpu().numpy(), Gp)
+    assert np.array_equal(Xs[:, :P], Xc.cpu().numpy()) and np.array_equal(Vs[:, :P], Vc.cpu().numpy())
+    Xo, Vo = oracle.step.step(X, V, G, mask, W.astype(np.float64), float(np.float32(0.1)),
+                              float(np.float32(0.9)), order)
+    assert rel_err(Vs[:, :P], Vo) <= TOL
+    assert rel_err(Xs[:, :P], Xo) <= TOL
+
+
+def test_strided_step_rejects_short_stride():
+    n, m, P = 2, 2, 64
+    X = torch.zeros(n, 60, dtype=torch.float32, device=DEV)
+    G = torch.zeros(n, m, 60, dtype=torch.float32, device=DEV)
+    with pytest.raises(nb.NbsgdError) as e:
+        _lib.step_strided(X, X.clone(), G, P, np.ones((n, m)), nb.w_ring(n), 0.1, 0.9, 0)
+    assert e.value.status == _lib.E_SHAPE
+
+
 @pytest.mark.parametrize("n,m,P", [(4, 4, 1030), (8, 16, 4098), (16, 4, 999), (3, 2, 5)])
 def test_unfused_stages_and_compositions(n, m, P):
     rng = np.random.default_rng(P)

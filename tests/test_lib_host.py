@@ -256,3 +256,22 @@ def test_matcha_set_get_and_errors():
             g.optimize(budget, iters)
         assert e.value.status == _lib.E_ARG
     g.close()
+
+
+def test_row_stride_rule():
+    # P below 2^22 floats: unpadded; else k * 2^22 with k = ceil(P / 2^22),
+    # a power-of-two k moved to the next integer (k = 1 -> 3)
+    u = 1 << 22
+    for P, want in ((0, 0), (1, 1), (10_000, 10_000), (u - 1, u - 1), (u, 3 * u), (u + 1, 3 * u),
+                    (2 * u + 1, 3 * u), (3 * u, 3 * u), (4 * u, 5 * u), (11_200_000, 3 * u),
+                    (23_500_000, 6 * u), (138_000_000, 33 * u), (8 * u + 1, 9 * u)):
+        ld = nb._lib.row_stride(P)
+        assert ld == want, (P, ld, want)
+        assert ld >= P
+        if P >= u:
+            k = ld // u
+            assert ld % u == 0 and k & (k - 1) != 0
+    with pytest.raises(nb.NbsgdError) as e:
+        nb._lib.row_stride(-1)
+    assert e.value.status == _lib.E_SHAPE
+    assert _lib.load().nbsgd_row_stride(5, None) == _lib.E_ARG
