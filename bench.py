@@ -120,6 +120,68 @@ def bench_mlp(args):
         "eval_loss_after": loss}), flush=True)
 
 
+def bench_unfused(args):
+    """The unfused stages on the same workload (nbsgd_accumulate, nbsgd_mix,
+    nbsgd_update; mix-then-step composition): per-kernel HIP-event times and
+    achieved bandwidth against each kernel's algorithmic bytes.  Contiguous
+    rows (these calls take [n][P])."""
+    import torch
+
+    from paper_2211_00889_amd import _lib, runner
+    from synth import device as synth_device
+    from synth import workloads
+
+    wl = workloads.get(args.workload)
+    n, m, P = wl.n, wl.m, wl.P
+    dev = torch.device("cuda:0")
+    X = torch.empty((n, P), dtype=torch.float32, device=dev)
+    Y = torch.empty_like(X)
+    V = torch.zeros_like(X)
+    Gbar = torch.empty_like(X)
+    G = torch.empty((n, m, P), dtype=torch.float32, device=dev)
+    synth_device.fill_normal(X, wl.seed, workloads.STREAM_X, wl.x_std)
+    synth_device.fill_normal(G, wl.seed, workloads.STREAM_G, wl.g_std)
+    sched = runner.Schedule(wl)
+    mixer = runner.Mixer(wl.mixing, n, wl.seed, wl.matcha_degree, wl.matcha_budget)
+    stream = torch.cuda.current_stream(dev)
+    names = ("k_accumulate", "k_mix", "k_update")
+    ms = {k: [] for k in names}
+    nbytes = {k: [] for k in names}
+    for k in range(args.warmup + args.steps):
+        mask, counts, _, _ = sched.mask(k)
+        W = mixer.w(k)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        _lib.accumulate(G, mask, Gbar)
+        ev[1].record(stream)
+        _lib.mix(X, W, Y)
+        ev[2].record(stream)
+        _lib.update(Y, V, Gbar, counts, m, wl.lr, wl.momentum)
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        X, Y = Y, X
+        if k >= args.warmup:
+            c = int(counts.sum())
+            for i, (name, b) in enumerate(zip(names, (4 * P * (c + n), 4 * P * 2 * n, 4 * P * 5 * n))):
+                ms[name].append(ev[i].elapsed_time(ev[i + 1]))
+                nbytes[name].append(b)
+    per = {}
+    for name in names:
+        t = float(np.mean(ms[name]))
+        per[name] = {"ms_mean": t, "alg_bytes_per_launch_mean": float(np.mean(nbytes[name])),
+                     "achieved_GBs": float(np.sum(nbytes[name]) / (np.sum(ms[name]) * 1e-3) / 1e9),
+                     "frac": float(np.sum(nbytes[name]) / (np.sum(ms[name]) * 1e-3) / 1e9 / PEAK_HBM_GBS)}
+    total_ms = float(sum(np.sum(ms[k]) for k in names) / args.steps)
+    print(json.dumps({
+        "metric": "unfused stages (accumulate, mix, update): per-kernel achieved HBM GB/s",
+        "value": n * P / (total_ms * 1e-3), "unit": "learner-param updates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": total_ms,
+        "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "n_learners": n, "minibatches": m, "P": P,
+                   "mixing": wl.mixing, "composition": "accumulate, mix, update"},
+        "kernels": per}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -127,6 +189,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="resnet18")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time the three unfused stages instead of the fused step")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--calibration-copy", action="store_true",
                     help="after the timed steps, run one plain 1 GiB device copy (torch's copy "
@@ -140,6 +204,9 @@ def main():
 
     if args.workload == "mlp":
         bench_mlp(args)
+        return
+    if args.unfused:
+        bench_unfused(args)
         return
 
     import torch
