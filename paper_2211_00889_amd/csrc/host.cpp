@@ -1,6 +1,6 @@
-// Host half of libnbsgd: the simulated straggler schedule, mixing-matrix
-// builders (uniform, ring, MATCHA), argument checks and the thread-local error
-// text.  Built with g++ -ffp-contract=off so every fp64 operation of the
+// Host half of libnbsgd: the simulated straggler schedule, the uniform and
+// ring mixing matrices, the local shuffle, argument checks and the
+// thread-local error text (MATCHA is in matcha.cpp).  Built with g++ -ffp-contract=off so every fp64 operation of the
 // schedule is a single IEEE operation in source order and log/pow are the
 // platform libm's.
 #include <math.h>
@@ -9,10 +9,7 @@
 #include <string.h>
 
 #include <algorithm>
-#include <new>
-#include <set>
 #include <string>
-#include <utility>
 #include <vector>
 
 #include "internal.h"
@@ -69,7 +66,6 @@ constexpr uint64_t kMul0 = 0xD2E7470EE14C6C93ull;
 constexpr uint64_t kMul1 = 0xCA5A826395121157ull;
 constexpr uint64_t kBump0 = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kBump1 = 0xBB67AE8584CAA73Bull;
-
 
 struct Philox4x64 {
   uint64_t v[4];
@@ -129,7 +125,7 @@ extern "C" nbsgd_status nbsgd_sample_mask(uint64_t seed, uint64_t step, int32_t 
        !(d->slow_prob <= 1.0)))
     return fail(NBSGD_E_ARG, "random slow-down needs slow_factor >= 1 and slow_prob in [0, 1]");
 
-  double finish[NBSGD_MAX_LEARNERS][NBSGD_MAX_MINIBATCHES];
+  double finish[NBSGD_MAX_LEARNERS][NBSGD_MAX_MINIBATCHES] = {};
   for (int32_t i = 0; i < n; ++i) {
     double s = (i == d->slow_learner) ? d->slow_factor : 1.0;
     if (d->slow_learner == NBSGD_SLOW_RANDOM) {
@@ -194,8 +190,6 @@ extern "C" nbsgd_status nbsgd_w_ring(int32_t n, float* W) {
   }
   return NBSGD_OK;
 }
-
-
 
 extern "C" const char* nbsgd_last_error(void) { return g_error.c_str(); }
 

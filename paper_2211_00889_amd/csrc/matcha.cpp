@@ -9,7 +9,6 @@
 // connectivity of the expected graph under the budget, and the alpha that
 // minimises the spectral norm of E[W^T W] - J/n.
 #include <math.h>
-#include <string.h>
 
 #include <algorithm>
 #include <new>

@@ -2,8 +2,11 @@
 // unfused stages (accumulate, mix, update), with their argument checks.
 //
 // Data layout (all fp32, row-major, caller-owned HBM):
-//   X, V  [n][P]      replicas and momentum buffers, learner-major
-//   G     [n][m][P]   per-mini-batch gradients
+//   X, V  [n][ld]     replicas and momentum buffers, learner-major
+//   G     [n][m][ld]  per-mini-batch gradients
+// with rows ld >= P floats apart: the first P floats of a row are the
+// parameters and the rest is never touched (ld = P except in the strided
+// fused step).
 // Every kernel works on column tiles: the mix couples learners, never
 // columns, so a workgroup that holds all n rows of its columns can update X in
 // place.  Rows are streamed as VEC-wide vectors (VEC = 4 when P % 4 == 0, else
