@@ -14,9 +14,16 @@ from ._lib import (  # noqa: F401
     NbsgdError,
     accumulate,
     load,
+    minibatch_indices,
     mix,
+    mlp_grad,
+    mlp_loss,
+    mlp_param_count,
+    mlp_workspace_bytes,
+    row_stride,
     sample_mask,
     step,
+    step_strided,
     update,
     w_allreduce,
     w_ring,
