@@ -87,9 +87,9 @@ typedef enum { NBSGD_DELAY_CONST = 0, NBSGD_DELAY_EXP = 1, NBSGD_DELAY_LOMAX = 2
 typedef struct {
   int32_t kind;        /* nbsgd_delay_kind */
   double base;         /* >= 0 */
-  double param;        /* EXP: rate > 0; LOMAX: shape > 0; CONST: ignored */
+  double param;        /* EXP: rate > 0; LOMAX: shape > 0 (finite); CONST: ignored */
   int32_t slow_learner;
-  double slow_factor;  /* > 0; >= 1 for NBSGD_SLOW_RANDOM */
+  double slow_factor;  /* finite, > 0; >= 1 for NBSGD_SLOW_RANDOM */
   double slow_prob;    /* NBSGD_SLOW_RANDOM only: in [0, 1] */
 } nbsgd_delay;
 
@@ -218,7 +218,11 @@ nbsgd_status nbsgd_w_ring(int32_t n, float *W);
  * and alpha = 1 / (degree + 1).
  * nbsgd_matcha_create: builds the graph; *out is owned by the caller and
  *   released with nbsgd_matcha_destroy.  Errors: NBSGD_E_ARG, NBSGD_E_SHAPE
- *   (no such regular graph), NBSGD_E_UNSUPPORTED.
+ *   (no such regular graph: n < 2, degree outside [1, n), n * degree odd,
+ *   degree 1 with n > 2; or none drawn in 100,000 attempts: a pairing is
+ *   simple with probability about exp(-(degree^2 - 1) / 4), so degrees of 7
+ *   and more, and graphs close to complete, usually end here),
+ *   NBSGD_E_UNSUPPORTED.
  * nbsgd_matcha_w: W of iteration `step`; n_active (nullable) receives the
  *   number of active matchings.
  * nbsgd_matcha_matchings: edges_uvq int32[3*E] as (u, v, matching) with u < v

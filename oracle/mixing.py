@@ -70,6 +70,8 @@ def random_regular_graph(seed: int, n: int, degree: int, max_attempts: int = 100
     """
     if n < 2 or degree < 1 or degree >= n or (n * degree) % 2:
         raise ValueError("no simple regular graph with these n and degree")
+    if degree == 1 and n > 2:
+        raise ValueError("a 1-regular graph (a perfect matching) is connected only on 2 nodes")
     H = n * degree
     for attempt in range(max_attempts):
         half = list(range(H))

@@ -113,13 +113,13 @@ extern "C" nbsgd_status nbsgd_sample_mask(uint64_t seed, uint64_t step, int32_t 
   if (!d || !mask || !counts) return fail(NBSGD_E_ARG, "d, mask and counts must not be null");
   if (d->kind < NBSGD_DELAY_CONST || d->kind > NBSGD_DELAY_LOMAX)
     return fail(NBSGD_E_ARG, "unknown delay kind %d", d->kind);
-  if (d->kind != NBSGD_DELAY_CONST && !(d->param > 0.0))
-    return fail(NBSGD_E_ARG, "delay param %g must be > 0", d->param);
+  if (d->kind != NBSGD_DELAY_CONST && (!(d->param > 0.0) || !isfinite(d->param)))
+    return fail(NBSGD_E_ARG, "delay param %g must be finite and > 0", d->param);
   if (!(d->base >= 0.0) || !isfinite(d->base)) return fail(NBSGD_E_ARG, "delay base must be >= 0");
   if (d->slow_learner < NBSGD_SLOW_RANDOM || d->slow_learner >= n)
     return fail(NBSGD_E_ARG, "slow_learner=%d must be in [-2, n)", d->slow_learner);
-  if (d->slow_learner >= 0 && !(d->slow_factor > 0.0))
-    return fail(NBSGD_E_ARG, "slow_factor %g must be > 0", d->slow_factor);
+  if (d->slow_learner >= 0 && (!(d->slow_factor > 0.0) || !isfinite(d->slow_factor)))
+    return fail(NBSGD_E_ARG, "slow_factor %g must be finite and > 0", d->slow_factor);
   if (d->slow_learner == NBSGD_SLOW_RANDOM &&
       (!(d->slow_factor >= 1.0) || !isfinite(d->slow_factor) || !(d->slow_prob >= 0.0) ||
        !(d->slow_prob <= 1.0)))

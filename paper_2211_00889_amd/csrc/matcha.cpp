@@ -193,6 +193,8 @@ extern "C" nbsgd_status nbsgd_matcha_create(uint64_t seed, int32_t n, int32_t de
   if (nbsgd_status st = check_nm(n, 1)) return st;
   if (n < 2 || degree < 1 || degree >= n || (n * degree) % 2)
     return fail(NBSGD_E_SHAPE, "no simple %d-regular graph on %d nodes", degree, n);
+  if (degree == 1 && n > 2)  // a perfect matching is connected only on two nodes
+    return fail(NBSGD_E_SHAPE, "no connected 1-regular graph on %d nodes", n);
   const int32_t H = n * degree;
   std::vector<int32_t> half(H);
   std::vector<std::pair<int32_t, int32_t>> edges;
