@@ -35,6 +35,29 @@ METRIC = "learner-param updates/sec and achieved HBM GB/s (% peak) for fused nbs
 UNIT = "learner-param updates/s"
 
 
+def copy_context(nbytes, dev, reps: int = 5):
+    """A plain device copy of ``nbytes`` (read ``nbytes``, write ``nbytes``):
+    the bandwidth an elementwise kernel reaches at the step's footprint."""
+    import torch
+
+    n = max(1, nbytes // 4)
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    best = float("inf")
+    for _ in range(reps):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        dst.copy_(src)
+        e.record()
+        torch.cuda.synchronize()
+        best = min(best, s.elapsed_time(e) * 1e-3)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"kernel": "torch copy_", "bytes_moved": 8 * n, "GBs": 8 * n / best / 1e9,
+            "frac": 8 * n / best / 1e9 / PEAK_HBM_GBS}
+
+
 def kernel_code_sha256(path):
     """sha256 of a source file without its // comments and blank lines: the
     key of a committed counter summary, which stays valid while only
@@ -101,8 +124,9 @@ def cpu_baseline(wl, budget_s: float = 15.0, cols: int = 1 << 19):
 def bench_mlp(args):
     """End-to-end MLP workload: per iteration the schedule, the shuffled
     indices, the per-mini-batch gradients on the matrix cores and the fused
-    step.  Prints one JSON line with finished training samples per second and
-    the algorithmic GEMM work; per-kernel times come from rocprofv3."""
+    step.  Prints one JSON line with finished training samples per second,
+    the algorithmic GEMM work and the device-time split between the gradient
+    kernels and the step; per-kernel times come from rocprofv3."""
     import torch
 
     from paper_2211_00889_amd import runner
@@ -121,6 +145,17 @@ def bench_mlp(args):
         finished += int(counts.sum())
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    # the split between the gradient kernels and the step, from device events
+    # in a separate pass (events inside the timed loop would slow it)
+    stream = torch.cuda.current_stream(dev)
+    events, split_finished = [], 0
+    k0 = args.warmup + args.steps
+    for k in range(k0, k0 + min(args.steps, 20)):
+        split_finished += int(r.step(k, stream, events=events)[1].sum())
+    torch.cuda.synchronize()
+    grad_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in events]))
+    step_ms = float(np.mean([b.elapsed_time(c) for _, b, c in events]))
+    split_flop = 2 * 2 * wl.batch * wl.d_in * wl.hidden * split_finished / len(events)
     loss = float(r.evaluate().mean().cpu())
     gemm_flop = 2 * 2 * wl.batch * wl.d_in * wl.hidden * finished  # forward and dW1 GEMMs
     print(json.dumps({
@@ -131,6 +166,9 @@ def bench_mlp(args):
         "config": {"workload": wl.name, "n_learners": wl.n, "minibatches": wl.m, "batch": wl.batch,
                    "P": wl.P, "mean_finished_per_step": finished / args.steps},
         "layer1_gemm_tflop_per_step": gemm_flop / args.steps / 1e12,
+        "split_ms": {"gradients": grad_ms, "step": step_ms, "iterations": len(events)},
+        "gradient_tflops": split_flop / (grad_ms * 1e-3) / 1e12,
+        "gradient_frac_of_bf16_dense_peak": split_flop / (grad_ms * 1e-3) / 2.5e15,
         "eval_loss_after": loss}), flush=True)
 
 
@@ -245,8 +283,11 @@ def main():
     sum_counts = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    plan_s = []
     for i in range(K):
+        t_plan = time.perf_counter()
         mask, counts, _, W = r.plan(args.warmup + i)
+        plan_s.append(time.perf_counter() - t_plan)
         starts[i].record(stream)
         r.launch(mask, W)
         ends[i].record(stream)
@@ -276,6 +317,7 @@ def main():
                    "mixing": wl.mixing, "order": wl.order, "delay": wl.delay.kind,
                    "lr": wl.lr, "momentum": wl.momentum,
                    "mean_finished_per_step": float(np.mean(sum_counts))},
+        "host_plan_us": float(np.mean(plan_s) * 1e6),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": None,
                      "kernel": "k_step", "kernel_ms_mean": float(kern_ms.mean()),
@@ -289,6 +331,7 @@ def main():
         out["roofline"]["traffic_dispatches"] = f"{rec['dispatches']} launches, steps {rec['steps']}"
     del r
     torch.cuda.empty_cache()
+    out["copy_context"] = copy_context(int(alg_bytes.mean()) // 2, dev)
     if args.calibration_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)

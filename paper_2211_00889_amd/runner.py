@@ -150,14 +150,16 @@ class MlpRunner:
         self.order = _ORDER[wl.order]
         self.w_mean = _lib.w_allreduce(wl.n)
 
-    def step(self, k: int, stream=None, blocking: bool = False):
+    def step(self, k: int, stream=None, blocking: bool = False, events=None):
         """Iteration k; returns (mask, counts, seconds): the finished mask, the
         finished counts and the iteration's simulated wall time.  Non-blocking
         (Alg. 2): the schedule's mask, time T_step (the terminal signal, or a
         forced first mini-batch if later).  ``blocking``: the D-PSGD baseline
         on the same W, every learner finishes all m mini-batches and the
         iteration waits for the slowest, T_sync.  The finished mini-batches'
-        losses are left in ``self.losses`` (index i*m + j)."""
+        losses are left in ``self.losses`` (index i*m + j).  ``events``: a
+        list that receives three recorded device events (before the
+        gradients, between gradients and step, after the step)."""
         wl = self.wl
         mask, counts, _, timing = self.schedule.mask(k)
         seconds = float(timing[2])
@@ -166,9 +168,21 @@ class MlpRunner:
             counts = np.full_like(counts, wl.m)
             seconds = float(timing[1])
         idx = _lib.minibatch_indices(wl.seed, k, wl.n, wl.m, wl.batch, wl.shard)
+        W = self.mixer.w(k)
+        ev = None
+        if events is not None:
+            import torch
+
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            ev[0].record(stream)
         _lib.mlp_grad(self.X, wl.m, self.dims, self.data, self.labels, idx, mask, self.G, self.losses,
                       self.workspace, stream)
-        _lib.step(self.X, self.V, self.G, mask, self.mixer.w(k), wl.lr, wl.momentum, self.order, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        _lib.step(self.X, self.V, self.G, mask, W, wl.lr, wl.momentum, self.order, stream)
+        if ev is not None:
+            ev[2].record(stream)
+            events.append(ev)
         return mask, counts, seconds
 
     def evaluate(self, stream=None):
