@@ -128,6 +128,40 @@ def test_strided_step_matches_oracle_and_leaves_padding(n, m, P, ld, order):
     assert rel_err(Xs[:, :P], Xo) <= TOL
 
 
+def test_random_shapes_sweep():
+    """24 seeded random (n, m, P, ld, order, mask, W) cases through the strided
+    fused step: parity with the oracle, bitwise equality with the contiguous
+    call, padding untouched."""
+    rng = np.random.default_rng(2024)
+    pad = np.float32(-7.5)
+    for case in range(24):
+        n, m = int(rng.integers(1, 17)), int(rng.integers(1, 65))
+        P = int(rng.integers(1, 3000))
+        ld = P + int(rng.integers(0, 9))
+        order = int(rng.integers(0, 2))
+        X, V, G = _inputs(rng, n, m, P)
+        mask = _random_mask(rng, n, m, prefix=bool(rng.integers(0, 2)))
+        W = _birkhoff_w(rng, n, terms=int(rng.integers(1, 4)))
+        _say(f"random case {case}: n={n} m={m} P={P} ld={ld} order={order}")
+        Xp = np.full((n, ld), pad, np.float32)
+        Vp = np.full((n, ld), pad, np.float32)
+        Gp = np.full((n, m, ld), pad, np.float32)
+        Xp[:, :P], Vp[:, :P], Gp[:, :, :P] = X, V, G
+        Xd, Vd, Gd = _dev(Xp), _dev(Vp), _dev(Gp)
+        _lib.step_strided(Xd, Vd, Gd, P, mask, W, 0.05, 0.8, order)
+        Xc, Vc = _dev(X), _dev(V)
+        nb.step(Xc, Vc, _dev(G), mask, W, 0.05, 0.8, order)
+        torch.cuda.synchronize()
+        Xs, Vs = Xd.cpu().numpy(), Vd.cpu().numpy()
+        assert (Xs[:, P:] == pad).all() and (Vs[:, P:] == pad).all(), case
+        assert np.array_equal(Xs[:, :P], Xc.cpu().numpy()), case
+        assert np.array_equal(Vs[:, :P], Vc.cpu().numpy()), case
+        Xo, Vo = oracle.step.step(X, V, G, mask, W.astype(np.float64), float(np.float32(0.05)),
+                                  float(np.float32(0.8)), order)
+        assert rel_err(Vs[:, :P], Vo) <= TOL, case
+        assert rel_err(Xs[:, :P], Xo) <= TOL, case
+
+
 def test_strided_step_rejects_short_stride():
     n, m, P = 2, 2, 64
     X = torch.zeros(n, 60, dtype=torch.float32, device=DEV)
