@@ -156,6 +156,9 @@ def bench_mlp(args):
     grad_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in events]))
     step_ms = float(np.mean([b.elapsed_time(c) for _, b, c in events]))
     split_flop = 2 * 2 * wl.batch * wl.d_in * wl.hidden * split_finished / len(events)
+    # the fused step's algorithmic bytes (finished G rows once, X and V read
+    # and written once) over its event time
+    step_bytes = 4 * r.P * (split_finished / len(events) + 4 * wl.n)
     loss = float(r.evaluate().mean().cpu())
     gemm_flop = 2 * 2 * wl.batch * wl.d_in * wl.hidden * finished  # forward and dW1 GEMMs
     print(json.dumps({
@@ -164,9 +167,10 @@ def bench_mlp(args):
         "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps, "higher_is_better": True,
         "dtype": "bf16 GEMM inputs, fp32 accumulation and step", "data": "synthetic CIFAR-shaped",
         "config": {"workload": wl.name, "n_learners": wl.n, "minibatches": wl.m, "batch": wl.batch,
-                   "P": wl.P, "mean_finished_per_step": finished / args.steps},
+                   "P": wl.P, "row_stride": r.ld, "mean_finished_per_step": finished / args.steps},
         "layer1_gemm_tflop_per_step": gemm_flop / args.steps / 1e12,
         "split_ms": {"gradients": grad_ms, "step": step_ms, "iterations": len(events)},
+        "step_gbps": step_bytes / (step_ms * 1e-3) / 1e9,
         "gradient_tflops": split_flop / (grad_ms * 1e-3) / 1e12,
         "gradient_frac_of_bf16_dense_peak": split_flop / (grad_ms * 1e-3) / 2.5e15,
         "eval_loss_after": loss}), flush=True)

@@ -185,13 +185,19 @@ nbsgd_status nbsgd_step_strided(float *X, float *V, const float *G, int64_t ld,
                                 int64_t P, float lr, float momentum, int32_t order, void *stream);
 
 /* Row stride (in floats) to allocate X, V and G with for nbsgd_step_strided:
- * P when P < 2^22, else k * 2^22 with k = ceil(P / 2^22), or the next
- * integer that is not a power of two when k is one (k = 1 gives 3), so every
- * row starts on a 16 MiB boundary without a power-of-two stride.  Measured on
- * MI355X for the fused step: the HBM throughput depends on where the rows
- * start relative to each other (the DRAM address mapping); this stride raised
- * the sustained rate of the 11.2M-, 23.5M- and 138M-parameter workloads by
- * 3-6% (k = 3, 6, 33), whereas a power-of-two stride lowered it by up to 8%.
+ *   P <= 2^20:          P (no padding);
+ *   2^20 < P <= 2^22:   the next power of two, 2^21 or 2^22;
+ *   P > 2^22:           k * 2^22 with k = ceil(P / 2^22), or k + 1 when k is
+ *                       a power of two, so every row starts on a 16 MiB
+ *                       boundary without a power-of-two stride.
+ * Measured on MI355X for the fused step: the HBM throughput depends on where
+ * the rows start relative to each other (the DRAM address mapping).  Above
+ * 2^22 this stride raised the sustained rate of the 11.2M-, 23.5M- and
+ * 138M-parameter workloads by 3-6% (k = 3, 6, 33), whereas a power-of-two
+ * stride lowered it by up to 8%; between 2^20 and 2^22 the power-of-two
+ * stride was the best or close to the best of the strides tried, 0-15% above
+ * unpadded rows.  The padding costs memory (up to twice the rows' size in the
+ * middle band), never traffic.
  * Errors: NBSGD_E_ARG (null ld), NBSGD_E_SHAPE (P < 0).                    */
 nbsgd_status nbsgd_row_stride(int64_t P, int64_t *ld);
 
@@ -314,6 +320,18 @@ nbsgd_status nbsgd_mlp_grad(const float *X, int32_t n, int32_t m, const nbsgd_ml
                             const float *data, const int32_t *labels, int64_t n_samples,
                             const int32_t *idx, const uint8_t *mask, float *G, float *losses,
                             void *workspace, size_t workspace_bytes, void *stream);
+
+/* nbsgd_mlp_grad on rows `ld` floats apart, the layout of nbsgd_step_strided:
+ * replica i is read from X + i*ld and mini-batch (i, j) written to
+ * G + (i*m + j)*ld; only the first P floats of a row are read or written.
+ * X needs (n-1)*ld + P floats and G (n*m-1)*ld + P.  ld must be a multiple
+ * of 4 and >= P (NBSGD_E_SHAPE).  nbsgd_mlp_grad is this call with ld = P.
+ * Errors: as nbsgd_mlp_grad.                                                */
+nbsgd_status nbsgd_mlp_grad_strided(const float *X, int64_t ld, int32_t n, int32_t m,
+                                    const nbsgd_mlp_shape *s, const float *data,
+                                    const int32_t *labels, int64_t n_samples, const int32_t *idx,
+                                    const uint8_t *mask, float *G, float *losses, void *workspace,
+                                    size_t workspace_bytes, void *stream);
 
 /* Mean cross-entropy of one parameter vector on `count` samples, in batches
  * of 32: losses[k] = mean loss of samples idx[32k .. 32k+31] (same precision

@@ -17,6 +17,7 @@ from ._lib import (  # noqa: F401
     minibatch_indices,
     mix,
     mlp_grad,
+    mlp_grad_strided,
     mlp_loss,
     mlp_param_count,
     mlp_workspace_bytes,

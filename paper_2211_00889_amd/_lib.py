@@ -29,7 +29,7 @@ EXPORTS = ("nbsgd_sample_mask", "nbsgd_accumulate", "nbsgd_mix", "nbsgd_update",
            "nbsgd_matcha_matchings", "nbsgd_matcha_set", "nbsgd_matcha_get", "nbsgd_matcha_optimize",
            "nbsgd_matcha_destroy", "nbsgd_mlp_param_count",
            "nbsgd_mlp_workspace_bytes", "nbsgd_minibatch_indices", "nbsgd_mlp_grad",
-           "nbsgd_mlp_loss", "nbsgd_last_error")
+           "nbsgd_mlp_grad_strided", "nbsgd_mlp_loss", "nbsgd_last_error")
 
 
 class NbsgdError(RuntimeError):
@@ -87,6 +87,9 @@ def load():
         "nbsgd_mlp_grad": [_c_void_p, _i32, _i32, ctypes.POINTER(MlpShape), _c_void_p, _c_void_p, _i64,
                            _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, ctypes.c_size_t,
                            _c_void_p],
+        "nbsgd_mlp_grad_strided": [_c_void_p, _i64, _i32, _i32, ctypes.POINTER(MlpShape), _c_void_p,
+                                   _c_void_p, _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                   _c_void_p, ctypes.c_size_t, _c_void_p],
         "nbsgd_mlp_loss": [_c_void_p, ctypes.POINTER(MlpShape), _c_void_p, _c_void_p, _i64, _c_void_p,
                            _i32, _c_void_p, _c_void_p, ctypes.c_size_t, _c_void_p],
     }
@@ -319,16 +322,42 @@ def _ws(t):
     return _c_void_p(t.data_ptr()), t.numel() * t.element_size()
 
 
-def mlp_grad(X, m: int, dims, data, labels, idx, mask, G, losses, workspace, stream=None):
-    """dims = (d_in, hidden, classes); idx host int32 [n, m, 32]; mask host [n, m]."""
+def _mlp_grad_args(X, m, dims, data, labels, idx, mask, G, losses, ld):
     n = X.shape[0]
+    if X.dim() != 2 or X.shape[1] != ld or tuple(G.shape) != (n, m, ld):
+        raise ValueError(f"X must be [n, {ld}] and G [n, m, {ld}]")
+    if losses.numel() < n * m:
+        raise ValueError("losses must hold n*m entries")
     idx = np.ascontiguousarray(np.asarray(idx), dtype=np.int32)
-    mask = _u8(mask, (n, m))
+    if idx.size != n * m * 32:
+        raise ValueError("idx must hold n*m*32 sample indices")
+    if data.dim() != 2 or data.shape[1] != dims[0] or labels.numel() < data.shape[0]:
+        raise ValueError("data must be [n_samples, d_in] with a label per sample")
+    return n, idx, _u8(mask, (n, m))
+
+
+def mlp_grad(X, m: int, dims, data, labels, idx, mask, G, losses, workspace, stream=None):
+    """dims = (d_in, hidden, classes); X [n, P]; G [n, m, P]; idx host int32
+    [n, m, 32]; mask host [n, m]."""
+    n, idx, mask = _mlp_grad_args(X, m, dims, data, labels, idx, mask, G, losses,
+                                  mlp_param_count(*dims))
     ws, ws_bytes = _ws(workspace)
     _check(load().nbsgd_mlp_grad(_dev(X, "X"), n, m, ctypes.byref(_shape(*dims)), _dev(data, "data"),
                                  _i32_dev(labels, "labels"), data.shape[0], _host_ptr(idx),
                                  _host_ptr(mask), _dev(G, "G"), _dev(losses, "losses"), ws, ws_bytes,
                                  _stream(X, stream)))
+
+
+def mlp_grad_strided(X, m: int, dims, data, labels, idx, mask, G, losses, workspace, stream=None):
+    """nbsgd_mlp_grad on padded rows: X [n, ld], G [n, m, ld] (the layout of
+    step_strided); the first P columns of each row are the parameters."""
+    ld = X.shape[-1]
+    n, idx, mask = _mlp_grad_args(X, m, dims, data, labels, idx, mask, G, losses, ld)
+    ws, ws_bytes = _ws(workspace)
+    _check(load().nbsgd_mlp_grad_strided(_dev(X, "X"), ld, n, m, ctypes.byref(_shape(*dims)),
+                                         _dev(data, "data"), _i32_dev(labels, "labels"),
+                                         data.shape[0], _host_ptr(idx), _host_ptr(mask), _dev(G, "G"),
+                                         _dev(losses, "losses"), ws, ws_bytes, _stream(X, stream)))
 
 
 def mlp_loss(params, dims, data, labels, idx, losses, workspace, stream=None):

@@ -19,7 +19,8 @@
 //
 // Flat parameter layout of a replica: W1[d_in][hidden], b1[hidden],
 // W2[hidden][classes], b2[classes], then zeros up to a multiple of 4 floats,
-// so every replica row and every G row starts 16-byte aligned.
+// so every replica row and every G row starts 16-byte aligned (rows are ld
+// floats apart, ld >= P a multiple of 4; ld = P unless the caller pads them).
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -46,7 +47,8 @@ constexpr int kFeatBlock = 128;  // d_in features per k_mlp_wgrad workgroup
 
 struct Dims {
   int32_t d_in, hidden, classes;
-  int64_t P;                     // padded parameters per replica (row length of X and G)
+  int64_t P;                     // padded parameters per replica
+  int64_t ld;                    // floats from one row of X (and of G) to the next, >= P
   int64_t off_b1, off_w2, off_b2, off_pad;
 };
 
@@ -152,7 +154,7 @@ __global__ void __launch_bounds__(512)
   const uint32_t item = L.w[M.first[li] + (g - M.off[li]) % tiles_i];
   const int slot_a = item_slot_a(item), slot_b = item_slot_b(item);
   const int rows = slot_b >= 0 ? 64 : 32;
-  const float* prm = X + (int64_t)item_learner(item) * d.P;
+  const float* prm = X + (int64_t)item_learner(item) * d.ld;
   const int H = d.hidden, C = d.classes;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = wave >> 2, wr = wave & 3;
@@ -299,7 +301,7 @@ __global__ void __launch_bounds__(256)
   __shared__ int ys[kBatch];
   const uint32_t item = L.w[blockIdx.x];
   const int slot = item_slot_a(item);
-  const float* prm = X + (int64_t)item_learner(item) * d.P;
+  const float* prm = X + (int64_t)item_learner(item) * d.ld;
   const int H = d.hidden, C = d.classes;
   const int blocks = H / 64;
   const int c0 = blockIdx.y * 64;
@@ -340,7 +342,7 @@ __global__ void __launch_bounds__(256)
       }
   }
   __syncthreads();
-  float* g = G + (int64_t)slot * d.P;
+  float* g = G + (int64_t)slot * d.ld;
   if (blockIdx.y == 0) {
     if (tid == 0) {
       float s = 0.0f;
@@ -454,7 +456,7 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
   for (int ft = 0; ft < kFeatBlock / 16; ++ft)
     fb[ft] = *reinterpret_cast<const bf16x8*>(&At[(16 * ft + (lane & 15)) * kLda + 8 * (lane >> 4)]);
-  float* g = G + (int64_t)slot * d.P + (int64_t)(f0 + (lane & 15)) * H + 4 * (lane >> 4);
+  float* g = G + (int64_t)slot * d.ld + (int64_t)(f0 + (lane & 15)) * H + 4 * (lane >> 4);
 #pragma unroll
   for (int u = 0; u < kMaxHidden / 64; ++u) {
     const int ht = wave + 4 * u;
@@ -489,6 +491,7 @@ nbsgd_status check_shape(const nbsgd_mlp_shape* s, Dims* d) {
   d->off_b2 = d->off_w2 + (int64_t)s->hidden * s->classes;
   d->off_pad = d->off_b2 + s->classes;
   d->P = (d->off_pad + 3) & ~(int64_t)3;
+  d->ld = d->P;
   return NBSGD_OK;
 }
 
@@ -633,15 +636,20 @@ extern "C" nbsgd_status nbsgd_mlp_workspace_bytes(const nbsgd_mlp_shape* s, int6
   return NBSGD_OK;
 }
 
-extern "C" nbsgd_status nbsgd_mlp_grad(const float* X, int32_t n, int32_t m, const nbsgd_mlp_shape* s,
-                                       const float* data, const int32_t* labels, int64_t n_samples,
-                                       const int32_t* idx, const uint8_t* mask, float* G,
-                                       float* losses, void* workspace, size_t workspace_bytes,
-                                       void* stream) {
-  clear_error();
+namespace {
+
+nbsgd_status mlp_grad_impl(const float* X, int64_t ld, int32_t n, int32_t m,
+                           const nbsgd_mlp_shape* s, const float* data, const int32_t* labels,
+                           int64_t n_samples, const int32_t* idx, const uint8_t* mask, float* G,
+                           float* losses, void* workspace, size_t workspace_bytes, void* stream) {
   if (nbsgd_status st = check_nm(n, m)) return st;
   Dims d;
   if (nbsgd_status st = check_shape(s, &d)) return st;
+  if (ld == 0) ld = d.P;
+  if (ld < d.P || ld % 4)
+    return fail(NBSGD_E_SHAPE, "row stride %lld must be a multiple of 4 and at least P=%lld",
+                (long long)ld, (long long)d.P);
+  d.ld = ld;
   if (!X || !data || !labels || !idx || !mask || !G || !losses || !workspace)
     return fail(NBSGD_E_ARG, "null pointer argument");
   if (((uintptr_t)X | (uintptr_t)data | (uintptr_t)G | (uintptr_t)workspace) & 15)
@@ -669,6 +677,30 @@ extern "C" nbsgd_status nbsgd_mlp_grad(const float* X, int32_t n, int32_t m, con
   }
   if (count) launch_group<true>(mb, count, X, data, w, G, losses, d, st);
   return launch_err("nbsgd_mlp_grad");
+}
+
+}  // namespace
+
+extern "C" nbsgd_status nbsgd_mlp_grad(const float* X, int32_t n, int32_t m, const nbsgd_mlp_shape* s,
+                                       const float* data, const int32_t* labels, int64_t n_samples,
+                                       const int32_t* idx, const uint8_t* mask, float* G,
+                                       float* losses, void* workspace, size_t workspace_bytes,
+                                       void* stream) {
+  clear_error();
+  return mlp_grad_impl(X, 0, n, m, s, data, labels, n_samples, idx, mask, G, losses, workspace,
+                       workspace_bytes, stream);
+}
+
+extern "C" nbsgd_status nbsgd_mlp_grad_strided(const float* X, int64_t ld, int32_t n, int32_t m,
+                                               const nbsgd_mlp_shape* s, const float* data,
+                                               const int32_t* labels, int64_t n_samples,
+                                               const int32_t* idx, const uint8_t* mask, float* G,
+                                               float* losses, void* workspace,
+                                               size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (ld <= 0) return fail(NBSGD_E_SHAPE, "row stride %lld must be positive", (long long)ld);
+  return mlp_grad_impl(X, ld, n, m, s, data, labels, n_samples, idx, mask, G, losses, workspace,
+                       workspace_bytes, stream);
 }
 
 extern "C" nbsgd_status nbsgd_mlp_loss(const float* params, const nbsgd_mlp_shape* s,

@@ -448,9 +448,10 @@ void launch_step(float* X, float* V, const float* G, int64_t pv, int64_t ldv, in
                      V, G, pv, ldv, n, mu, S, W);
 }
 
-// Rows of 2^22 floats (16 MiB) or more start on 16 MiB boundaries when the
-// stride is a multiple of 2^22 floats (see nbsgd_row_stride).
+// Row strides of nbsgd_row_stride: rows longer than 2^22 floats (16 MiB)
+// start on 16 MiB boundaries; rows of 2^20 floats or fewer are not padded.
 constexpr int64_t kRowAlign = int64_t(1) << 22;
+constexpr int64_t kSmallRow = int64_t(1) << 20;
 
 // The fused step on rows `ld` floats apart (ld >= P).
 nbsgd_status step_impl(float* X, float* V, const float* G, int64_t ld, const uint8_t* mask,
@@ -513,12 +514,18 @@ extern "C" nbsgd_status nbsgd_row_stride(int64_t P, int64_t* ld) {
   clear_error();
   if (!ld) return fail(NBSGD_E_ARG, "ld is null");
   if (P < 0) return fail(NBSGD_E_SHAPE, "P=%lld is negative", (long long)P);
-  if (P < kRowAlign) {
+  if (P <= kSmallRow) {
     *ld = P;
     return NBSGD_OK;
   }
-  int64_t k = (P + kRowAlign - 1) / kRowAlign;  // rows of k * 2^22 floats
-  if ((k & (k - 1)) == 0) k = k == 1 ? 3 : k + 1;  // a power-of-two stride aliases
+  if (P <= kRowAlign) {  // the next power of two, 2^21 or 2^22
+    int64_t p2 = kSmallRow;
+    while (p2 < P) p2 <<= 1;
+    *ld = p2;
+    return NBSGD_OK;
+  }
+  int64_t k = (P + kRowAlign - 1) / kRowAlign;  // rows of k * 2^22 floats, k >= 2
+  if ((k & (k - 1)) == 0) ++k;  // a power-of-two stride aliases
   *ld = k * kRowAlign;
   return NBSGD_OK;
 }

@@ -59,7 +59,8 @@ class StepRunner:
     """Replicas X, momentum V and gradients G of one workload on a device.
 
     Rows are allocated ``ld = nbsgd_row_stride(P)`` floats apart (P itself
-    below 2^22, else a multiple of 2^22 so rows start on 16 MiB boundaries);
+    up to 2^20, the next power of two up to 2^22, else a multiple of 2^22 so
+    rows start on 16 MiB boundaries);
     ``X``, ``V`` and ``G`` are the [.., P] views of the parameters.  Every row
     holds the values the generator gives the contiguous [n, P] / [n, m, P]
     tensor (flat index row * P + column)."""
@@ -135,16 +136,22 @@ class MlpRunner:
         x0 = np.asarray(x0, dtype=np.float32)
         row = np.zeros(self.P, np.float32)  # the library's layout pads the vector with zeros
         row[:x0.size] = x0
-        self.X = torch.from_numpy(row).to(dev).repeat(wl.n, 1)
-        self.V = torch.zeros_like(self.X)
-        self.G = torch.zeros((wl.n, wl.m, self.P), dtype=torch.float32, device=dev)
+        # rows ld floats apart (the fused step's row stride); X, V, G view the
+        # first P columns
+        P, ld = self.P, _lib.row_stride(self.P)
+        self.ld = ld
+        self.Xrows = torch.zeros((wl.n, ld), dtype=torch.float32, device=dev)
+        self.Xrows[:, :P] = torch.from_numpy(row).to(dev)
+        self.Vrows = torch.zeros((wl.n, ld), dtype=torch.float32, device=dev)
+        self.Grows = torch.zeros((wl.n, wl.m, ld), dtype=torch.float32, device=dev)
+        self.X, self.V, self.G = self.Xrows[:, :P], self.Vrows[:, :P], self.Grows[:, :, :P]
         self.losses = torch.zeros(wl.n * wl.m, dtype=torch.float32, device=dev)
         self.eval_idx = wl.eval_indices()
         self.eval_losses = torch.zeros(len(self.eval_idx) // wl.batch, dtype=torch.float32, device=dev)
         rows = max(wl.n * wl.m * wl.batch, len(self.eval_idx))
         ws = _lib.mlp_workspace_bytes(*self.dims, rows)
         self.workspace = torch.empty((ws + 15) // 16 * 4, dtype=torch.float32, device=dev)
-        self.mean = torch.empty_like(self.X)
+        self.mean = torch.zeros_like(self.Xrows)
         self.mixer = Mixer(wl.mixing, wl.n, wl.seed)
         self.schedule = Schedule(wl)
         self.order = _ORDER[wl.order]
@@ -175,11 +182,12 @@ class MlpRunner:
 
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
             ev[0].record(stream)
-        _lib.mlp_grad(self.X, wl.m, self.dims, self.data, self.labels, idx, mask, self.G, self.losses,
-                      self.workspace, stream)
+        _lib.mlp_grad_strided(self.Xrows, wl.m, self.dims, self.data, self.labels, idx, mask,
+                              self.Grows, self.losses, self.workspace, stream)
         if ev is not None:
             ev[1].record(stream)
-        _lib.step(self.X, self.V, self.G, mask, W, wl.lr, wl.momentum, self.order, stream)
+        _lib.step_strided(self.Xrows, self.Vrows, self.Grows, self.P, mask, W, wl.lr, wl.momentum,
+                          self.order, stream)
         if ev is not None:
             ev[2].record(stream)
             events.append(ev)
@@ -188,7 +196,8 @@ class MlpRunner:
     def evaluate(self, stream=None):
         """Loss of the average replica (the method's output) on the fixed
         evaluation samples, per batch of 32 (device tensor)."""
-        _lib.mix(self.X, self.w_mean, self.mean, stream)
-        _lib.mlp_loss(self.mean[0], self.dims, self.data, self.labels, self.eval_idx, self.eval_losses,
+        # whole rows: the padding columns hold zeros and average to zeros
+        _lib.mix(self.Xrows, self.w_mean, self.mean, stream)
+        _lib.mlp_loss(self.mean[0, :self.P], self.dims, self.data, self.labels, self.eval_idx, self.eval_losses,
                       self.workspace, stream)
         return self.eval_losses

@@ -68,20 +68,22 @@ def test_matcha_create_any_arguments(seed, n, degree):
 
 
 @SETTINGS
-@given(P=st.integers(-5, 1 << 40))
+@given(P=st.one_of(st.integers(-5, 1 << 40), st.integers((1 << 20) - 2, (1 << 22) + 2)))
 def test_row_stride_any_size(P):
     try:
         ld = nb.row_stride(P)
     except nb.NbsgdError as e:
         assert e.status == _lib.E_SHAPE and P < 0
         return
-    u = 1 << 22
+    u, s = 1 << 22, 1 << 20
     assert ld >= P >= 0
-    if P < u:
+    if P <= s:
         assert ld == P
+    elif P <= u:
+        assert ld & (ld - 1) == 0 and ld < 2 * P
     else:
         k = ld // u
-        assert ld % u == 0 and k & (k - 1) != 0 and ld - P <= 2 * u
+        assert ld % u == 0 and k & (k - 1) != 0 and ld - P < 2 * u
 
 
 @SETTINGS

@@ -69,14 +69,19 @@ def test_grad_small_shape_every_entry(tiny):
 
 
 def test_grad_full_shape_sampled_entries():
+    """The full shape in the runner's launch configuration: padded rows
+    (row_stride(P) = 2^21 floats apart) through nbsgd_mlp_grad_strided."""
     wl = workloads.MLP
     s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
     A, y, x0 = _data(wl)
     r = runner.MlpRunner(wl, DEV, A, y, x0)
+    assert r.ld == 1 << 21 and r.ld > r.P
     mask, counts, _, _ = r.schedule.mask(0)
     idx = _lib.minibatch_indices(wl.seed, 0, wl.n, wl.m, wl.batch, wl.shard)
-    _say(f"mlp grad full shape finished={int(mask.sum())}")
-    _lib.mlp_grad(r.X, wl.m, r.dims, r.data, r.labels, idx, mask, r.G, r.losses, r.workspace)
+    _say(f"mlp grad full shape finished={int(mask.sum())} ld={r.ld}")
+    r.Grows.fill_(7.0)
+    _lib.mlp_grad_strided(r.Xrows, wl.m, r.dims, r.data, r.labels, idx, mask, r.Grows, r.losses,
+                          r.workspace)
     torch.cuda.synchronize()
     L = r.losses.cpu().numpy().reshape(wl.n, wl.m)
     finished = list(zip(*np.nonzero(mask)))
@@ -84,6 +89,49 @@ def test_grad_full_shape_sampled_entries():
         g, loss = oracle.mlp.grad(x0, A[idx[i, j]], y[idx[i, j]], s, BF16)
         assert rel_err_blocks(r.G[i, j].cpu().numpy(), g, mlp_blocks(*r.dims)) <= TOL_BF16
         assert abs(L[i, j] - loss) <= TOL_BF16 * abs(loss)
+    # every finished row: the layout padding inside P is zero, the row
+    # padding beyond P untouched; unfinished rows untouched
+    tail = r.Grows[:, :, s.n_params:].cpu().numpy()
+    for i in range(wl.n):
+        for j in range(wl.m):
+            if mask[i, j]:
+                assert (tail[i, j, :r.P - s.n_params] == 0).all()
+                assert (tail[i, j, r.P - s.n_params:] == 7.0).all()
+            else:
+                assert (tail[i, j] == 7.0).all() and (r.G[i, j, :64] == 7.0).all()
+
+
+def test_grad_strided_rows_match_contiguous_small_shape(tiny):
+    """nbsgd_mlp_grad_strided on rows 36 floats longer than P: the same bits
+    as nbsgd_mlp_grad on contiguous rows, the row padding never read (NaN in
+    X) nor written (sentinel in G)."""
+    wl, A, y, x0 = tiny
+    s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
+    rng = np.random.default_rng(7)
+    X = (x0[None, :] + 0.05 * rng.standard_normal((wl.n, s.n_params))).astype(np.float32)
+    mask = (rng.random((wl.n, wl.m)) < 0.7).astype(np.uint8)
+    mask[2] = 0
+    mask[0, 0] = 1
+    idx = rng.integers(0, wl.n_samples, size=(wl.n, wl.m, wl.batch)).astype(np.int32)
+    r = runner.MlpRunner(wl, DEV, A, y, x0)
+    P, ld = r.P, r.P + 36
+    Xc = torch.from_numpy(pad_cols(X, P)).to(DEV)
+    Gc = torch.full((wl.n, wl.m, P), 7.0, dtype=torch.float32, device=DEV)
+    Lc = torch.full((wl.n * wl.m,), -1.0, dtype=torch.float32, device=DEV)
+    Xs = torch.full((wl.n, ld), float("nan"), dtype=torch.float32, device=DEV)
+    Xs[:, :P] = Xc
+    Gs = torch.full((wl.n, wl.m, ld), 7.0, dtype=torch.float32, device=DEV)
+    Ls = torch.full((wl.n * wl.m,), -1.0, dtype=torch.float32, device=DEV)
+    _say(f"mlp grad strided ld={ld} P={P} finished={int(mask.sum())}")
+    _lib.mlp_grad(Xc, wl.m, r.dims, r.data, r.labels, idx, mask, Gc, Lc, r.workspace)
+    _lib.mlp_grad_strided(Xs, wl.m, r.dims, r.data, r.labels, idx, mask, Gs, Ls, r.workspace)
+    torch.cuda.synchronize()
+    assert torch.equal(Gs[:, :, :P], Gc) and torch.equal(Ls, Lc)
+    assert (Gs[:, :, P:] == 7.0).all()
+    Gn = Gc.cpu().numpy()
+    for (i, j) in list(zip(*np.nonzero(mask)))[:3]:
+        g, _ = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
+        assert rel_err_blocks(Gn[i, j], g, mlp_blocks(*r.dims)) <= TOL_BF16, (i, j)
 
 
 def test_training_small_shape_matches_oracle(tiny):

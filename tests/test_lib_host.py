@@ -208,6 +208,29 @@ def test_mlp_grad_rejects_bad_indices_before_launch():
     assert rc == _lib.E_ARG and b"workspace" in lib.nbsgd_last_error()
 
 
+def test_mlp_grad_strided_checks_row_stride_before_launch():
+    lib = _lib.load()
+    shape = _lib.MlpShape(128, 64, 10, 32)
+    P = _lib.mlp_param_count(128, 64, 10)
+    n, m = 2, 2
+    idx = np.zeros(n * m * 32, np.int32)
+    idx[5] = 100  # out of range for n_samples = 100
+    mask = np.ones(n * m, np.uint8)
+    ws = _lib.mlp_workspace_bytes(128, 64, 10, n * m * 32)
+    p = ctypes.c_void_p(0x100000)
+
+    def call(ld):
+        return lib.nbsgd_mlp_grad_strided(p, ld, n, m, ctypes.byref(shape), p, p, 100,
+                                          idx.ctypes.data_as(ctypes.c_void_p),
+                                          mask.ctypes.data_as(ctypes.c_void_p), p, p, p, ws, None)
+
+    for bad in (0, -4, P - 4, P + 2, P + 1):
+        assert call(bad) == _lib.E_SHAPE, bad
+        assert b"row stride" in lib.nbsgd_last_error()
+    for good in (P, P + 4, 1 << 21):  # accepted: the sample list is checked next
+        assert call(good) == _lib.E_ARG and b"position 5" in lib.nbsgd_last_error()
+
+
 @pytest.mark.parametrize("seed,n,degree,budget", [(0, 16, 3, 0.5), (1, 10, 4, 0.3), (3, 12, 2, 1.0)])
 def test_matcha_optimize_matches_oracle(seed, n, degree, budget):
     g = nb.Matcha(seed, n, degree)
@@ -259,16 +282,18 @@ def test_matcha_set_get_and_errors():
 
 
 def test_row_stride_rule():
-    # P below 2^22 floats: unpadded; else k * 2^22 with k = ceil(P / 2^22),
-    # a power-of-two k moved to the next integer (k = 1 -> 3)
-    u = 1 << 22
-    for P, want in ((0, 0), (1, 1), (10_000, 10_000), (u - 1, u - 1), (u, 3 * u), (u + 1, 3 * u),
-                    (2 * u + 1, 3 * u), (3 * u, 3 * u), (4 * u, 5 * u), (11_200_000, 3 * u),
-                    (23_500_000, 6 * u), (138_000_000, 33 * u), (8 * u + 1, 9 * u)):
+    # P up to 2^20 floats: unpadded; up to 2^22: the next power of two; else
+    # k * 2^22 with k = ceil(P / 2^22), a power-of-two k moved to k + 1
+    u, s = 1 << 22, 1 << 20
+    for P, want in ((0, 0), (1, 1), (10_000, 10_000), (s - 1, s - 1), (s, s), (s + 1, 2 * s),
+                    (1_578_508, 2 * s), (2 * s, 2 * s), (2 * s + 1, u), (3_000_000, u), (u - 1, u),
+                    (u, u), (u + 1, 3 * u), (2 * u, 3 * u), (2 * u + 1, 3 * u), (3 * u, 3 * u),
+                    (4 * u, 5 * u), (11_200_000, 3 * u), (23_500_000, 6 * u),
+                    (138_000_000, 33 * u), (8 * u + 1, 9 * u)):
         ld = nb._lib.row_stride(P)
         assert ld == want, (P, ld, want)
         assert ld >= P
-        if P >= u:
+        if P > u:
             k = ld // u
             assert ld % u == 0 and k & (k - 1) != 0
     with pytest.raises(nb.NbsgdError) as e:
