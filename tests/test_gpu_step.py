@@ -275,7 +275,7 @@ def test_tiny_workload_every_step():
             assert rel_err(r.X.cpu().numpy(), Xo) <= TOL, k
 
 
-def _windows(P, seed, k=8, width=4096, edge=65536):
+def _windows(P, seed, k=16, width=4096, edge=65536):
     rng = np.random.default_rng(seed)
     cols = [np.arange(0, min(edge, P)), np.arange(max(0, P - edge), P)]
     for s in rng.integers(0, P - width, size=k):
