@@ -135,6 +135,7 @@ __global__ void __launch_bounds__(512)
               const int32_t* __restrict__ idx, float* __restrict__ Z1, float* __restrict__ Zp,
               int64_t zp_stride, Dims d, FwdMap M, List L) {
   constexpr int kKc = 64;        // K per staged chunk
+  constexpr int kDepth = 2;      // chunks loaded ahead of the one being staged
   constexpr int kLdb = kKc + 8;  // bf16 per transposed row (16-byte aligned, padded)
   constexpr int kLdh = 64 + 1;
   constexpr int kLdp = 64 + 1;   // padded partial-sum row
@@ -164,10 +165,10 @@ __global__ void __launch_bounds__(512)
   // instruction reads whole 256-byte row pieces)
   const int sa = htid >> 4, sq = 4 * (htid & 15);
   const float* wsrc = prm + (int64_t)(4 * sa) * H + c0 + sq;
-  // this lane's A row (tile row 16 wr + lane % 16) and K offset within a 32-step
+  // this lane's A row (tile row 16 wr + lane % 16) and first k (4 per lane group)
   const int lr = 16 * wr + (lane & 15);
   const int sample = mma ? idx[(lr < 32 ? slot_a : slot_b) * kBatch + (lr & 31)] : 0;
-  const float* arow = data + (int64_t)sample * d.d_in + 8 * (lane >> 4);
+  const float* arow = data + (int64_t)sample * d.d_in + 4 * (lane >> 4);
   __bf16* my_bs = Bs + half * 2 * kStage;
 
   struct Regs {
@@ -180,12 +181,20 @@ __global__ void __launch_bounds__(512)
     if (mma) {
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        R.a[u] = *reinterpret_cast<const f32x4*>(arow + k0 + 4 * (u & 1) + 32 * (u >> 1));
+        R.a[u] = *reinterpret_cast<const f32x4*>(arow + k0 + 16 * u);
     }
   };
   bf16x8 fa[2], fn[2];  // A fragments (K steps 0, 1) of the current and the next chunk
+  // K order within a 64-deep chunk: the MFMA sums over its 32 K slots in any
+  // order, so slot (step ks, lane group g, element t) takes k = 32 ks +
+  // 16 (t / 4) + 4 g + t % 4.  Then a lane's A values of one load are 4
+  // consecutive k, and the four lane groups of a row read 64 contiguous bytes.
+  // The staged chunk is [unit][k] in 16-byte pieces, piece 4 ks + g holding
+  // that fragment's 8 k; piece c of unit u sits at position c ^ ((u / 8) % 8)
+  // of its row, so that the fragment reads spread over all LDS banks.
   auto stage = [&](const Regs& R, int buf) {
-    __bf16* b = my_bs + buf * kStage + 4 * sa;
+    __bf16* b = my_bs + buf * kStage + 8 * ((4 * (sa >> 3) + (sa & 3)) ^ ((sq >> 3) & 7)) +
+                4 * ((sa >> 2) & 1);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const uint2 v = {pack_bf16(R.w[0][t], R.w[1][t]), pack_bf16(R.w[2][t], R.w[3][t])};
@@ -207,39 +216,44 @@ __global__ void __launch_bounds__(512)
   for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto multiply = [&](int buf) {
     if (!mma) return;
-    const __bf16* bs = my_bs + buf * kStage + (lane & 15) * kLdb + 8 * (lane >> 4);
+    const __bf16* bs = my_bs + buf * kStage + (lane & 15) * kLdb;
+    const int piece = lane >> 4, swz = (lane & 15) >> 3;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
-        const bf16x8 fb = *reinterpret_cast<const bf16x8*>(bs + 16 * ct * kLdb + 32 * ks);
+        const int col = 8 * ((piece + 4 * ks) ^ (swz + 2 * ct));
+        const bf16x8 fb = *reinterpret_cast<const bf16x8*>(bs + 16 * ct * kLdb + col);
         acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[ks], fb, acc[ct], 0, 0, 0);
       }
   };
   // half h takes chunks h, h+2, ...: S of them (d_in % 128 == 0, so every
-  // half has the same count); chunk s of this half is 2 s + h
+  // half has the same count); chunk s of this half is 2 s + h.  Register set
+  // c % kDepth holds chunk c from its load until it is staged.
   const int S = d.d_in / (2 * kKc);
-  Regs R0, R1;
-  load(R0, half);
-  if (S > 1) load(R1, 2 + half);
-  stage(R0, 0);
+  Regs R[kDepth];
+#pragma unroll
+  for (int c = 0; c < kDepth; ++c)
+    if (c < S) load(R[c], 2 * c + half);
+  stage(R[0], 0);
   fa[0] = fn[0];
   fa[1] = fn[1];
-  if (S > 2) load(R0, 4 + half);
+  if (kDepth < S) load(R[0], 2 * kDepth + half);
   __syncthreads();
-  // step s: multiply chunk s (LDS buffer s % 2); stage chunk s+1 from the
-  // register set that holds it and refill that set with chunk s+3
+  // step s: multiply chunk s (LDS buffer s % 2); stage chunk s+1 from its
+  // register set and refill that set with chunk s+1+kDepth
   auto step = [&](int s, Regs& Rn) {
     multiply(s & 1);
     if (s + 1 < S) stage(Rn, (s + 1) & 1);
-    if (s + 3 < S) load(Rn, 2 * (s + 3) + half);
+    if (s + 1 + kDepth < S) load(Rn, 2 * (s + 1 + kDepth) + half);
     __syncthreads();
     fa[0] = fn[0];
     fa[1] = fn[1];
   };
-  for (int s = 0; s < S; s += 2) {
-    step(s, R1);                 // chunk s+1 is in R1
-    if (s + 1 < S) step(s + 1, R0);  // chunk s+2 is in R0
+  for (int s = 0; s < S; s += kDepth) {
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j)
+      if (s + j < S) step(s + j, R[(j + 1) % kDepth]);
   }
 
   // half 1 hands its sums to half 0 through LDS
@@ -438,8 +452,12 @@ __global__ void __launch_bounds__(256)
   }
   {
     // rows 2p, 2p+1 (p = tid / 16) of the mini-batch, features 4q .. 4q+3 and
-    // 64 + 4q .. (q = tid % 16): packed pairs of rows into At[f][r]
+    // 64 + 4q .. (q = tid % 16): packed pairs of rows into At[f][r].  A row
+    // of At is four 16-byte pieces of 8 samples; piece c of feature f sits at
+    // position c ^ ((f / 16) % 4), so that these writes (features four apart)
+    // and the fragment reads both spread over all LDS banks.
     const int p = tid >> 4, q = 4 * (tid & 15);
+    const int pw = 4 * ((p >> 2) ^ ((q >> 4) & 3)) + (p & 3);  // dword of row pair p
     const float* s0 = data + (int64_t)idx[row0 + 2 * p] * d.d_in + f0 + q;
     const float* s1 = data + (int64_t)idx[row0 + 2 * p + 1] * d.d_in + f0 + q;
     uint32_t* a32 = reinterpret_cast<uint32_t*>(At);
@@ -448,14 +466,15 @@ __global__ void __launch_bounds__(256)
       const f32x4 x0 = *reinterpret_cast<const f32x4*>(s0 + 64 * h);
       const f32x4 x1 = *reinterpret_cast<const f32x4*>(s1 + 64 * h);
 #pragma unroll
-      for (int t = 0; t < 4; ++t) a32[((64 * h + q + t) * kLda + 2 * p) >> 1] = pack_bf16(x0[t], x1[t]);
+      for (int t = 0; t < 4; ++t) a32[((64 * h + q + t) * kLda >> 1) + pw] = pack_bf16(x0[t], x1[t]);
     }
   }
   __syncthreads();
   bf16x8 fb[kFeatBlock / 16];
 #pragma unroll
   for (int ft = 0; ft < kFeatBlock / 16; ++ft)
-    fb[ft] = *reinterpret_cast<const bf16x8*>(&At[(16 * ft + (lane & 15)) * kLda + 8 * (lane >> 4)]);
+    fb[ft] = *reinterpret_cast<const bf16x8*>(
+        &At[(16 * ft + (lane & 15)) * kLda + 8 * ((lane >> 4) ^ (ft & 3))]);
   float* g = G + (int64_t)slot * d.ld + (int64_t)(f0 + (lane & 15)) * H + 4 * (lane >> 4);
 #pragma unroll
   for (int u = 0; u < kMaxHidden / 64; ++u) {
