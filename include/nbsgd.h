@@ -38,6 +38,7 @@
 #ifndef NBSGD_H
 #define NBSGD_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
