@@ -254,7 +254,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the simulated learners are replicas in one "
-              f"GPU's HBM and this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              f"GPU's HBM and there is no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
 
