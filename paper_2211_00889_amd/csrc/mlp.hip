@@ -5,10 +5,11 @@
 //
 // Every GEMM input is rounded to bf16 (round to nearest even, the hardware
 // conversion) and multiplied with fp32 accumulation:
-//   k_mlp_fwd    Z1 = A W1 + b1 on MFMA 16x16x32 (full K per tile), then in
-//                the epilogue H = bf16(relu(Z1)) and this tile's 64-unit share
-//                of the logits, sum_h H W2 (vector ALUs; N = classes is below
-//                one 16-wide MFMA tile)
+//   k_mlp_fwd_sk  partial Z1 = A W1 over one slice of d_in, per 128-row x
+//                 128-unit tile, on MFMA 16x16x32 (both operands staged in LDS)
+//   k_mlp_fwd_sum Z1 = sum of the slices + b1, then H = bf16(relu(Z1)) and
+//                 each 64-unit block's share of the logits, sum_h H W2 (vector
+//                 ALUs; N = classes is below one 16-wide MFMA tile)
 //   k_mlp_head   logits = sum of the shares + b2, softmax-CE, dZ2; per 64
 //                hidden units dW2 = H^T dZ2, dZ1 = (dZ2 W2^T) * [Z1 > 0], db1;
 //                db2 and the loss once per mini-batch
@@ -54,8 +55,9 @@ struct Dims {
 
 // One launch's work items, word k = learner << 24 | slot_a << 12 | (slot_b + 1).
 // A slot indexes the sample list (slot * 32 ..), the workspace rows and the
-// loss output; k_mlp_fwd takes up to two mini-batches of one learner per item
-// (slot_b + 1 == 0: one), the other kernels one.  Read as 32-bit words only.
+// loss output; k_mlp_fwd_sum takes up to two mini-batches of one learner per
+// item (slot_b + 1 == 0: one), the other kernels one.  Read as 32-bit words
+// only.
 struct List {
   int32_t count;
   uint32_t w[kMaxList];
@@ -106,10 +108,10 @@ __global__ void __launch_bounds__(256)
   ylab[slot * kBatch + r] = y < 0 ? 0 : (y >= classes ? classes - 1 : y);
 }
 
-// Forward work items: the (tile, 64-unit block) pairs in order learner,
+// Slice-sum work items: the (tile, 64-unit block) pairs in order learner,
 // unit block, tile, cut into 8 contiguous ranges, one per XCD (workgroup b
-// runs on XCD b % 8), so the workgroups that share a tile's sample rows or a
-// learner's W1 block share one L2.  Item g of learner i is unit block
+// runs on XCD b % 8), so the workgroups of one learner mostly share one L2.
+// Item g of learner i is unit block
 // (g - off[i]) / tiles_i of tile first[i] + (g - off[i]) % tiles_i.
 struct FwdMap {
   int32_t n;                // learners present
@@ -119,35 +121,171 @@ struct FwdMap {
 };
 static_assert(sizeof(FwdMap) <= 180, "forward map grew: recheck the kernel-argument budget");
 
-// Z1 for up to 64 rows (the mini-batches slot_a, slot_b of one learner) and
-// the 64 hidden units c0 .. c0+63, over the whole of d_in.  Eight waves:
-// wave w takes rows 16 (w % 4) .. +15, all 64 units (four 16x16
-// accumulators) and the K half w / 4 (64-deep chunks h, h+2, ...); its A
-// fragments come straight from the sample rows.  Each half stages its W1
-// chunks through LDS, transposed to [unit][k] in bf16 so that a B fragment
-// is one 16-byte read.  Loads run two chunks ahead: while chunk s is
-// multiplied, chunk s+1 is in LDS-bound registers and s+2 in flight.  The
-// halves' sums are added in half order.  Epilogue: Z1 (+ b1) to the
-// workspace, then this tile's share of the logits Zp[block][row][c] = sum
-// over its 64 units of bf16(relu(Z1)) bf16(W2).
+// Forward, split over d_in.  Work item: a quad (up to four mini-batches of one
+// learner, 128 rows), a block of 128 hidden units and one of S equal slices of
+// d_in (S = the largest divisor of d_in / 64 up to kSkMaxSlices).  Both operands
+// are staged through LDS in bf16 ([row][k] and [unit][k], padded rows), so a
+// 16-byte read is one MFMA fragment.  Eight waves: wave w takes rows
+// 32 (w % 4) .. +31 and units 64 (w / 4) .. +63 (2 x 4 accumulators).  The
+// partial sums go to slice s of the partial buffer; k_mlp_fwd_sum adds the
+// slices in slice order.
+constexpr int kSkRows = 128, kSkUnits = 128, kSkKc = 64, kSkLd = kSkKc + 8;
+constexpr int kSkMaxSlices = 4;
+struct SkMap {
+  int32_t n;              // learners present
+  int32_t S;              // K slices
+  int32_t ub;             // unit blocks
+  int32_t xcd_start[9];   // item range of each XCD
+  int32_t off[17];        // first work item of each learner (off[n] = total)
+  int32_t first[17];      // first list entry of each learner (first[n] = count)
+};
+static_assert(sizeof(List) + sizeof(Dims) + sizeof(SkMap) + 5 * 8 <= 4096,
+              "kernel arguments exceed 4 KiB");
+
 __global__ void __launch_bounds__(512)
-    k_mlp_fwd(const float* __restrict__ X, const float* __restrict__ data,
-              const int32_t* __restrict__ idx, float* __restrict__ Z1, float* __restrict__ Zp,
-              int64_t zp_stride, Dims d, FwdMap M, List L) {
-  constexpr int kKc = 64;        // K per staged chunk
-  constexpr int kDepth = 2;      // chunks loaded ahead of the one being staged
-  constexpr int kLdb = kKc + 8;  // bf16 per transposed row (16-byte aligned, padded)
-  constexpr int kLdh = 64 + 1;
-  constexpr int kLdp = 64 + 1;   // padded partial-sum row
-  constexpr int kStage = 64 * kLdb;  // bf16 per staging buffer
-  // 2 halves x 2 buffers of staging; after the K loop it holds half 1's sums
-  __shared__ __attribute__((aligned(16))) __bf16 Bs[2 * 2 * kStage];
-  __shared__ float Hs[64 * kLdh];
-  __shared__ float W2s[64 * kMaxClasses];
-  static_assert(64 * kLdp * 4 <= (int)sizeof(Bs), "partial sums exceed the staging space");
+    k_mlp_fwd_sk(const float* __restrict__ X, const float* __restrict__ data,
+                 const int32_t* __restrict__ idx, float* __restrict__ Zpart, int64_t part_stride,
+                 Dims d, SkMap M, List L) {
+  constexpr int kDepth = 2;  // chunks loaded ahead of the one being staged
+  __shared__ __attribute__((aligned(16))) __bf16 As[2][kSkRows * kSkLd];
+  __shared__ __attribute__((aligned(16))) __bf16 Ws[2][kSkUnits * kSkLd];
   const int xcd = blockIdx.x & 7;
   const int g = M.xcd_start[xcd] + (int)(blockIdx.x >> 3);
-  if (g >= M.xcd_start[xcd + 1]) return;  // uniform: the whole workgroup leaves
+  if (g >= M.xcd_start[xcd + 1]) return;  // uniform
+  int li = 0;
+  while (li + 1 < M.n && M.off[li + 1] <= g) ++li;
+  const int cnt = M.first[li + 1] - M.first[li];
+  const int quads = (cnt + 3) >> 2;
+  int local = g - M.off[li];
+  const int quad = local % quads;
+  local /= quads;
+  const int ubk = local % M.ub, s = local / M.ub;
+  const int e0 = M.first[li] + 4 * quad;         // first list entry of the quad
+  const int nmb = min(4, cnt - 4 * quad);
+  const int rows = kBatch * nmb;
+  const int H = d.hidden;
+  const int u0 = kSkUnits * ubk;
+  const int units = min(kSkUnits, H - u0);
+  const int kslice = d.d_in / M.S, nck = kslice / kSkKc;
+  const int kb = s * kslice;
+  const float* prm = X + (int64_t)item_learner(L.w[e0]) * d.ld;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave & 3, wu = wave >> 2;
+  const bool mma = 32 * wr < rows && 64 * wu < units;  // wave-uniform
+
+  // A staging: row tid / 4, k = 4 q + 16 j (+0..3), q = tid % 4
+  const int arow = tid >> 2, aq = tid & 3;
+  const bool alive = arow < rows;
+  const float* asrc = data;
+  if (alive) {
+    const int slot = item_slot_a(L.w[e0 + (arow >> 5)]);
+    asrc = data + (int64_t)idx[slot * kBatch + (arow & 31)] * d.d_in + kb + 4 * aq;
+  }
+  // W1 staging: k rows 4 wa .. +3, units 4 wq .. +3
+  const int wa = tid >> 5, wq = tid & 31;
+  const bool wlive = 4 * wq < units;
+  const float* wsrc = prm + (int64_t)(kb + 4 * wa) * H + u0 + 4 * wq;
+
+  struct Regs {
+    f32x4 a[4], w[4];
+  };
+  auto load = [&](Regs& R, int c) {
+    const int k0 = c * kSkKc;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      R.a[j] = alive ? *reinterpret_cast<const f32x4*>(asrc + k0 + 16 * j) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      R.w[r] = wlive ? *reinterpret_cast<const f32x4*>(wsrc + (int64_t)(k0 + r) * H)
+                     : f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+  auto stage = [&](const Regs& R, int buf) {
+    __bf16* a = As[buf] + arow * kSkLd + 4 * aq;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint2 v = {pack_bf16(R.a[j][0], R.a[j][1]), pack_bf16(R.a[j][2], R.a[j][3])};
+      *reinterpret_cast<uint2*>(a + 16 * j) = v;
+    }
+    __bf16* w = Ws[buf] + (4 * wq) * kSkLd + 4 * wa;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const uint2 v = {pack_bf16(R.w[0][t], R.w[1][t]), pack_bf16(R.w[2][t], R.w[3][t])};
+      *reinterpret_cast<uint2*>(w + t * kSkLd) = v;
+    }
+  };
+  f32x4 acc[2][4];
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc[f][u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto multiply = [&](int buf) {
+    if (!mma) return;
+    const __bf16* a = As[buf] + (32 * wr + (lane & 15)) * kSkLd + 8 * (lane >> 4);
+    const __bf16* w = Ws[buf] + (64 * wu + (lane & 15)) * kSkLd + 8 * (lane >> 4);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 fa[2];
+#pragma unroll
+      for (int f = 0; f < 2; ++f) fa[f] = *reinterpret_cast<const bf16x8*>(a + 16 * f * kSkLd + 32 * ks);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bf16x8 fb = *reinterpret_cast<const bf16x8*>(w + 16 * u * kSkLd + 32 * ks);
+#pragma unroll
+        for (int f = 0; f < 2; ++f)
+          acc[f][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[f], fb, acc[f][u], 0, 0, 0);
+      }
+    }
+  };
+  Regs R[kDepth];
+#pragma unroll
+  for (int c = 0; c < kDepth; ++c)
+    if (c < nck) load(R[c], c);
+  stage(R[0], 0);
+  if (kDepth < nck) load(R[0], kDepth);
+  __syncthreads();
+  // step c: multiply chunk c (buffer c % 2); stage chunk c+1 from its register
+  // set and refill that set with chunk c+1+kDepth
+  auto step = [&](int c, Regs& Rn) {
+    multiply(c & 1);
+    if (c + 1 < nck) stage(Rn, (c + 1) & 1);
+    if (c + 1 + kDepth < nck) load(Rn, c + 1 + kDepth);
+    __syncthreads();
+  };
+  for (int c = 0; c < nck; c += kDepth) {
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j)
+      if (c + j < nck) step(c + j, R[(j + 1) % kDepth]);
+  }
+  if (!mma) return;
+  float* out = Zpart + (int64_t)s * part_stride;
+#pragma unroll
+  for (int f = 0; f < 2; ++f) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int r = 32 * wr + 16 * f + 4 * (lane >> 4) + t;
+      if (r >= rows) continue;
+      const int slot = item_slot_a(L.w[e0 + (r >> 5)]);
+      float* o = out + ((int64_t)slot * kBatch + (r & 31)) * H + u0 + 64 * wu + (lane & 15);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) o[16 * u] = acc[f][u][t];
+    }
+  }
+}
+
+// Z1 = (sum of the S partial slices, in slice order) + b1 for the rows of a
+// tile (up to two mini-batches of one learner) and 64 hidden units, then this
+// tile's share of the logits Zp[block][row][c] = sum over its 64 units of
+// bf16(relu(Z1)) bf16(W2).
+__global__ void __launch_bounds__(256)
+    k_mlp_fwd_sum(const float* __restrict__ X, const float* __restrict__ Zpart, int64_t part_stride,
+                  int S, float* __restrict__ Z1, float* __restrict__ Zp, int64_t zp_stride, Dims d,
+                  FwdMap M, List L) {
+  constexpr int kLdh = 64 + 1;
+  __shared__ float Hs[64 * kLdh];
+  __shared__ float W2s[64 * kMaxClasses];
+  const int xcd = blockIdx.x & 7;
+  const int g = M.xcd_start[xcd] + (int)(blockIdx.x >> 3);
+  if (g >= M.xcd_start[xcd + 1]) return;
   int li = 0;
   while (li + 1 < M.n && M.off[li + 1] <= g) ++li;
   const int tiles_i = (M.off[li + 1] - M.off[li]) / (d.hidden / 64);
@@ -157,132 +295,35 @@ __global__ void __launch_bounds__(512)
   const int rows = slot_b >= 0 ? 64 : 32;
   const float* prm = X + (int64_t)item_learner(item) * d.ld;
   const int H = d.hidden, C = d.classes;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int half = wave >> 2, wr = wave & 3;
-  const int htid = tid & 255;  // thread index within the half
-  const bool mma = 16 * wr < rows;  // wave-uniform
-  // W1 staging: rows 4a .. 4a+3 of the chunk, units 4q .. 4q+3 (each load
-  // instruction reads whole 256-byte row pieces)
-  const int sa = htid >> 4, sq = 4 * (htid & 15);
-  const float* wsrc = prm + (int64_t)(4 * sa) * H + c0 + sq;
-  // this lane's A row (tile row 16 wr + lane % 16) and first k (4 per lane group)
-  const int lr = 16 * wr + (lane & 15);
-  const int sample = mma ? idx[(lr < 32 ? slot_a : slot_b) * kBatch + (lr & 31)] : 0;
-  const float* arow = data + (int64_t)sample * d.d_in + 4 * (lane >> 4);
-  __bf16* my_bs = Bs + half * 2 * kStage;
-
-  struct Regs {
-    f32x4 w[4], a[4];
-  };
-  auto load = [&](Regs& R, int chunk) {
-    const int k0 = chunk * kKc;
+  const int tid = threadIdx.x;
+  // thread: row tid / 4, units 4 (tid % 4) + 16 j, j = 0..3; every slice's
+  // loads are issued before the sums
+  const int r = tid >> 2, uq = 4 * (tid & 3);
+  if (r < rows) {
+    const int64_t at = ((int64_t)(r < 32 ? slot_a : slot_b) * kBatch + (r & 31)) * H + c0 + uq;
+    f32x4 p[kSkMaxSlices][4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) R.w[r] = *reinterpret_cast<const f32x4*>(wsrc + (int64_t)(k0 + r) * H);
-    if (mma) {
+    for (int q = 0; q < kSkMaxSlices; ++q)
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        R.a[u] = *reinterpret_cast<const f32x4*>(arow + k0 + 16 * u);
-    }
-  };
-  bf16x8 fa[2], fn[2];  // A fragments (K steps 0, 1) of the current and the next chunk
-  // K order within a 64-deep chunk: the MFMA sums over its 32 K slots in any
-  // order, so slot (step ks, lane group g, element t) takes k = 32 ks +
-  // 16 (t / 4) + 4 g + t % 4.  Then a lane's A values of one load are 4
-  // consecutive k, and the four lane groups of a row read 64 contiguous bytes.
-  // The staged chunk is [unit][k] in 16-byte pieces, piece 4 ks + g holding
-  // that fragment's 8 k; piece c of unit u sits at position c ^ ((u / 8) % 8)
-  // of its row, so that the fragment reads spread over all LDS banks.
-  auto stage = [&](const Regs& R, int buf) {
-    __bf16* b = my_bs + buf * kStage + 8 * ((4 * (sa >> 3) + (sa & 3)) ^ ((sq >> 3) & 7)) +
-                4 * ((sa >> 2) & 1);
+      for (int j = 0; j < 4; ++j)
+        p[q][j] = q < S ? *reinterpret_cast<const f32x4*>(Zpart + (int64_t)q * part_stride + at + 16 * j)
+                        : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const uint2 v = {pack_bf16(R.w[0][t], R.w[1][t]), pack_bf16(R.w[2][t], R.w[3][t])};
-      *reinterpret_cast<uint2*>(b + (sq + t) * kLdb) = v;
-    }
-    if (mma) {
+    for (int j = 0; j < 4; ++j) {
+      f32x4 z = p[0][j];
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
+      for (int q = 1; q < kSkMaxSlices; ++q)
+        if (q < S) z += p[q][j];
+      const f32x4 b = *reinterpret_cast<const f32x4*>(prm + d.off_b1 + c0 + uq + 16 * j);
+      z += b;
+      *reinterpret_cast<f32x4*>(Z1 + at + 16 * j) = z;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          fn[ks][t] = (__bf16)R.a[2 * ks][t];
-          fn[ks][t + 4] = (__bf16)R.a[2 * ks + 1][t];
-        }
-    }
-  };
-
-  f32x4 acc[4];
-#pragma unroll
-  for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto multiply = [&](int buf) {
-    if (!mma) return;
-    const __bf16* bs = my_bs + buf * kStage + (lane & 15) * kLdb;
-    const int piece = lane >> 4, swz = (lane & 15) >> 3;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int ct = 0; ct < 4; ++ct) {
-        const int col = 8 * ((piece + 4 * ks) ^ (swz + 2 * ct));
-        const bf16x8 fb = *reinterpret_cast<const bf16x8*>(bs + 16 * ct * kLdb + col);
-        acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[ks], fb, acc[ct], 0, 0, 0);
-      }
-  };
-  // half h takes chunks h, h+2, ...: S of them (d_in % 128 == 0, so every
-  // half has the same count); chunk s of this half is 2 s + h.  Register set
-  // c % kDepth holds chunk c from its load until it is staged.
-  const int S = d.d_in / (2 * kKc);
-  Regs R[kDepth];
-#pragma unroll
-  for (int c = 0; c < kDepth; ++c)
-    if (c < S) load(R[c], 2 * c + half);
-  stage(R[0], 0);
-  fa[0] = fn[0];
-  fa[1] = fn[1];
-  if (kDepth < S) load(R[0], 2 * kDepth + half);
-  __syncthreads();
-  // step s: multiply chunk s (LDS buffer s % 2); stage chunk s+1 from its
-  // register set and refill that set with chunk s+1+kDepth
-  auto step = [&](int s, Regs& Rn) {
-    multiply(s & 1);
-    if (s + 1 < S) stage(Rn, (s + 1) & 1);
-    if (s + 1 + kDepth < S) load(Rn, 2 * (s + 1 + kDepth) + half);
-    __syncthreads();
-    fa[0] = fn[0];
-    fa[1] = fn[1];
-  };
-  for (int s = 0; s < S; s += kDepth) {
-#pragma unroll
-    for (int j = 0; j < kDepth; ++j)
-      if (s + j < S) step(s + j, R[(j + 1) % kDepth]);
-  }
-
-  // half 1 hands its sums to half 0 through LDS
-  float* part = reinterpret_cast<float*>(Bs);  // [64][kLdp]
-  if (half == 1 && mma) {
-#pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-        part[(16 * wr + 4 * (lane >> 4) + t) * kLdp + 16 * ct + (lane & 15)] = acc[ct][t];
-  }
-  __syncthreads();
-  if (half == 0 && mma) {
-#pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
-      const int col = 16 * ct + (lane & 15);
-      const float b = prm[d.off_b1 + c0 + col];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int r = 16 * wr + 4 * (lane >> 4) + t;
-        const float z = acc[ct][t] + part[r * kLdp + col] + b;
-        Z1[((int64_t)(r < 32 ? slot_a : slot_b) * kBatch + (r & 31)) * H + c0 + col] = z;
-        Hs[r * kLdh + col] = bf16r(fmaxf(z, 0.0f));
-      }
+      for (int t = 0; t < 4; ++t) Hs[r * kLdh + uq + 16 * j + t] = bf16r(fmaxf(z[t], 0.0f));
     }
   }
-  for (int k = tid; k < 64 * C; k += 512) W2s[k] = bf16r(prm[d.off_w2 + (int64_t)c0 * C + k]);
+  for (int k = tid; k < 64 * C; k += 256) W2s[k] = bf16r(prm[d.off_w2 + (int64_t)c0 * C + k]);
   __syncthreads();
-  for (int o = tid; o < rows * C; o += 512) {
+  for (int o = tid; o < rows * C; o += 256) {
     const int r = o / C, c = o % C;
     float s = 0.0f;
     for (int h = 0; h < 64; ++h) s += Hs[r * kLdh + h] * W2s[h * C + c];
@@ -517,11 +558,13 @@ nbsgd_status check_shape(const nbsgd_mlp_shape* s, Dims* d) {
 size_t up256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 // sample list, labels, Z1 [rows][hidden] fp32, hidden/64 logit-share planes
-// [rows][16] fp32 and dZ1 [rows/32][hidden][32] bf16, each 256-byte aligned
+// [rows][16] fp32, dZ1 [rows/32][hidden][32] bf16 and kSkMaxSlices partial Z1
+// planes [rows][hidden] fp32, each 256-byte aligned
 size_t workspace_for(const Dims& d, int64_t rows) {
   return 2 * up256((size_t)rows * 4) + up256((size_t)rows * d.hidden * 4) +
          (size_t)(d.hidden / 64) * up256((size_t)rows * kMaxClasses * 4) +
-         up256((size_t)rows * d.hidden * 2);
+         up256((size_t)rows * d.hidden * 2) +
+         (size_t)kSkMaxSlices * up256((size_t)rows * d.hidden * 4);
 }
 
 struct Workspace {
@@ -531,6 +574,8 @@ struct Workspace {
   float* zp;
   int64_t zp_stride;  // floats between logit-share planes
   __bf16* dz1t;
+  float* part;        // partial Z1 of each d_in slice
+  int64_t part_stride;
 };
 
 Workspace carve(void* ws, const Dims& d, int64_t rows) {
@@ -546,6 +591,9 @@ Workspace carve(void* ws, const Dims& d, int64_t rows) {
   w.zp_stride = (int64_t)(up256((size_t)rows * kMaxClasses * 4) / 4);
   p += (size_t)(d.hidden / 64) * up256((size_t)rows * kMaxClasses * 4);
   w.dz1t = reinterpret_cast<__bf16*>(p);
+  p += up256((size_t)rows * d.hidden * 2);
+  w.part = reinterpret_cast<float*>(p);
+  w.part_stride = (int64_t)(up256((size_t)rows * d.hidden * 4) / 4);
   return w;
 }
 
@@ -588,6 +636,8 @@ nbsgd_status launch_err(const char* what) {
   return NBSGD_OK;
 }
 
+int item_learner_h(uint32_t w) { return (int)(w >> 24); }
+
 uint32_t item(int learner, int slot_a, int slot_b) {
   return ((uint32_t)learner << 24) | ((uint32_t)slot_a << 12) | (uint32_t)(slot_b + 1);
 }
@@ -625,8 +675,35 @@ void launch_group(const std::pair<int, int>* mb, int count, const float* X, cons
   M.first[M.n] = tiles.count;
   for (int x = 0; x <= 8; ++x) M.xcd_start[x] = (int32_t)((int64_t)x * total / 8);
   const int per_xcd = (total + 7) / 8;
-  hipLaunchKernelGGL(k_mlp_fwd, dim3(8 * per_xcd), dim3(512), 0, st, X, data, w.idx, w.z1, w.zp,
-                     w.zp_stride, d, M, tiles);
+  // forward over quads of each learner's entries in `items`, then the slice sums
+  SkMap K;
+  memset(&K, 0, sizeof K);
+  const int chunks = d.d_in / kSkKc;
+  K.S = 1;
+  for (int q = kSkMaxSlices; q >= 1; --q)
+    if (chunks % q == 0) {
+      K.S = q;
+      break;
+    }
+  K.ub = (d.hidden + kSkUnits - 1) / kSkUnits;
+  int sk_total = 0;
+  for (int k = 0; k < items.count; ++k) {
+    if (k == 0 || item_learner_h(items.w[k]) != item_learner_h(items.w[k - 1])) {
+      if (K.n > 0) sk_total += K.S * K.ub * ((k - K.first[K.n - 1] + 3) / 4);
+      K.off[K.n] = sk_total;
+      K.first[K.n] = k;
+      ++K.n;
+    }
+  }
+  sk_total += K.S * K.ub * ((items.count - K.first[K.n - 1] + 3) / 4);
+  K.off[K.n] = sk_total;
+  K.first[K.n] = items.count;
+  for (int x = 0; x <= 8; ++x) K.xcd_start[x] = (int32_t)((int64_t)x * sk_total / 8);
+  const int sk_per_xcd = (sk_total + 7) / 8;
+  hipLaunchKernelGGL(k_mlp_fwd_sk, dim3(8 * sk_per_xcd), dim3(512), 0, st, X, data, w.idx, w.part,
+                     w.part_stride, d, K, items);
+  hipLaunchKernelGGL(k_mlp_fwd_sum, dim3(8 * per_xcd), dim3(256), 0, st, X, w.part, w.part_stride,
+                     K.S, w.z1, w.zp, w.zp_stride, d, M, tiles);
   hipLaunchKernelGGL(k_mlp_head<BACKWARD>, dim3(items.count, BACKWARD ? nb : 1), dim3(256), 0, st, X,
                      w.ylab, w.z1, w.zp, w.zp_stride, w.dz1t, G, losses, d, items);
   if (BACKWARD)
