@@ -7,12 +7,10 @@
 // conversion) and multiplied with fp32 accumulation:
 //   k_mlp_fwd_sk  partial Z1 = A W1 over one slice of d_in, per 128-row x
 //                 128-unit tile, on MFMA 16x16x32 (both operands staged in LDS)
-//   k_mlp_fwd_sum Z1 = sum of the slices + b1, then H = bf16(relu(Z1)) and
-//                 each 64-unit block's share of the logits, sum_h H W2 (vector
-//                 ALUs; N = classes is below one 16-wide MFMA tile)
-//   k_mlp_head   logits = sum of the shares + b2, softmax-CE, dZ2; per 64
-//                hidden units dW2 = H^T dZ2, dZ1 = (dZ2 W2^T) * [Z1 > 0], db1;
-//                db2 and the loss once per mini-batch
+//   k_mlp_head    per mini-batch: Z1 = sum of the slices + b1, H =
+//                 bf16(relu(Z1)), logits = H W2 + b2 (MFMA, classes padded to
+//                 16), softmax-CE, dZ2; dZ1 = (dZ2 W2^T) * [Z1 > 0], db1, dW2 =
+//                 H^T dZ2 (MFMA), db2 and the loss
 //   k_mlp_wgrad  dW1 = A^T dZ1 on MFMA 16x16x32 (K = batch = 32), each lane
 //                storing four consecutive hidden units of one G row
 // MFMA 16x16x32 bf16 operand layout (lane l, t = 0..7): A[l % 16][8 (l / 16) + t],
@@ -41,7 +39,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBatch = 32;       // mini-batch size (the MFMA K of dW1)
 constexpr int kMaxHidden = 512;
-constexpr int kMaxClasses = 16;  // the logit shares are stored 16 wide
+constexpr int kMaxClasses = 16;  // classes fill one 16-wide MFMA tile
 constexpr int kMaxList = 896;    // mini-batches per launch (kernel-argument list)
 constexpr int kMaxEval = 512;    // batches of 32 per nbsgd_mlp_loss call
 constexpr int kFeatBlock = 128;  // d_in features per k_mlp_wgrad workgroup
@@ -53,11 +51,9 @@ struct Dims {
   int64_t off_b1, off_w2, off_b2, off_pad;
 };
 
-// One launch's work items, word k = learner << 24 | slot_a << 12 | (slot_b + 1).
-// A slot indexes the sample list (slot * 32 ..), the workspace rows and the
-// loss output; k_mlp_fwd_sum takes up to two mini-batches of one learner per
-// item (slot_b + 1 == 0: one), the other kernels one.  Read as 32-bit words
-// only.
+// One launch's mini-batches, word k = learner << 24 | slot << 12, sorted by
+// learner.  A slot indexes the sample list (slot * 32 ..), the workspace rows
+// and the loss output.  Read as 32-bit words only.
 struct List {
   int32_t count;
   uint32_t w[kMaxList];
@@ -75,13 +71,12 @@ struct IdxChunk {
 
 // kernel arguments are limited to 4 KiB: the list, the shapes, the forward
 // map and at most ten pointers or 64-bit scalars
-static_assert(sizeof(List) + sizeof(Dims) + 180 + 10 * 8 <= 4096, "kernel arguments exceed 4 KiB");
+static_assert(sizeof(List) + sizeof(Dims) + 10 * 8 <= 4096, "kernel arguments exceed 4 KiB");
 static_assert(sizeof(IdxChunk) + 32 <= 4096, "kernel arguments exceed 4 KiB");
 static_assert(kMaxList <= 4096 && kMaxEval <= 4096, "slots are packed in 16 bits");
 
 __device__ __forceinline__ int item_learner(uint32_t w) { return (int)(w >> 24); }
-__device__ __forceinline__ int item_slot_a(uint32_t w) { return (int)((w >> 12) & 0xfffu); }
-__device__ __forceinline__ int item_slot_b(uint32_t w) { return (int)(w & 0xfffu) - 1; }
+__device__ __forceinline__ int item_slot(uint32_t w) { return (int)((w >> 12) & 0xfffu); }
 
 __device__ __forceinline__ float bf16r(float x) { return (float)(__bf16)x; }
 
@@ -108,18 +103,6 @@ __global__ void __launch_bounds__(256)
   ylab[slot * kBatch + r] = y < 0 ? 0 : (y >= classes ? classes - 1 : y);
 }
 
-// Slice-sum work items: the (tile, 64-unit block) pairs in order learner,
-// unit block, tile, cut into 8 contiguous ranges, one per XCD (workgroup b
-// runs on XCD b % 8), so the workgroups of one learner mostly share one L2.
-// Item g of learner i is unit block
-// (g - off[i]) / tiles_i of tile first[i] + (g - off[i]) % tiles_i.
-struct FwdMap {
-  int32_t n;                // learners present
-  int32_t xcd_start[9];     // item range of each XCD
-  int32_t off[17];          // first item of each learner (off[n] = total)
-  int32_t first[17];        // first tile of each learner in the tile list
-};
-static_assert(sizeof(FwdMap) <= 180, "forward map grew: recheck the kernel-argument budget");
 
 // Forward, split over d_in.  Work item: a quad (up to four mini-batches of one
 // learner, 128 rows), a block of 128 hidden units and one of S equal slices of
@@ -127,7 +110,7 @@ static_assert(sizeof(FwdMap) <= 180, "forward map grew: recheck the kernel-argum
 // are staged through LDS in bf16 ([row][k] and [unit][k], padded rows), so a
 // 16-byte read is one MFMA fragment.  Eight waves: wave w takes rows
 // 32 (w % 4) .. +31 and units 64 (w / 4) .. +63 (2 x 4 accumulators).  The
-// partial sums go to slice s of the partial buffer; k_mlp_fwd_sum adds the
+// partial sums go to slice s of the partial buffer; k_mlp_head adds the
 // slices in slice order.
 constexpr int kSkRows = 128, kSkUnits = 128, kSkKc = 64, kSkLd = kSkKc + 8;
 constexpr int kSkMaxSlices = 4;
@@ -178,7 +161,7 @@ __global__ void __launch_bounds__(512)
   const bool alive = arow < rows;
   const float* asrc = data;
   if (alive) {
-    const int slot = item_slot_a(L.w[e0 + (arow >> 5)]);
+    const int slot = item_slot(L.w[e0 + (arow >> 5)]);
     asrc = data + (int64_t)idx[slot * kBatch + (arow & 31)] * d.d_in + kb + 4 * aq;
   }
   // W1 staging: k rows 4 wa .. +3, units 4 wq .. +3
@@ -264,7 +247,7 @@ __global__ void __launch_bounds__(512)
     for (int t = 0; t < 4; ++t) {
       const int r = 32 * wr + 16 * f + 4 * (lane >> 4) + t;
       if (r >= rows) continue;
-      const int slot = item_slot_a(L.w[e0 + (r >> 5)]);
+      const int slot = item_slot(L.w[e0 + (r >> 5)]);
       float* o = out + ((int64_t)slot * kBatch + (r & 31)) * H + u0 + 64 * wu + (lane & 15);
 #pragma unroll
       for (int u = 0; u < 4; ++u) o[16 * u] = acc[f][u][t];
@@ -272,112 +255,100 @@ __global__ void __launch_bounds__(512)
   }
 }
 
-// Z1 = (sum of the S partial slices, in slice order) + b1 for the rows of a
-// tile (up to two mini-batches of one learner) and 64 hidden units, then this
-// tile's share of the logits Zp[block][row][c] = sum over its 64 units of
-// bf16(relu(Z1)) bf16(W2).
-__global__ void __launch_bounds__(256)
-    k_mlp_fwd_sum(const float* __restrict__ X, const float* __restrict__ Zpart, int64_t part_stride,
-                  int S, float* __restrict__ Z1, float* __restrict__ Zp, int64_t zp_stride, Dims d,
-                  FwdMap M, List L) {
-  constexpr int kLdh = 64 + 1;
-  __shared__ float Hs[64 * kLdh];
-  __shared__ float W2s[64 * kMaxClasses];
-  const int xcd = blockIdx.x & 7;
-  const int g = M.xcd_start[xcd] + (int)(blockIdx.x >> 3);
-  if (g >= M.xcd_start[xcd + 1]) return;
-  int li = 0;
-  while (li + 1 < M.n && M.off[li + 1] <= g) ++li;
-  const int tiles_i = (M.off[li + 1] - M.off[li]) / (d.hidden / 64);
-  const int c0 = 64 * ((g - M.off[li]) / tiles_i);
-  const uint32_t item = L.w[M.first[li] + (g - M.off[li]) % tiles_i];
-  const int slot_a = item_slot_a(item), slot_b = item_slot_b(item);
-  const int rows = slot_b >= 0 ? 64 : 32;
-  const float* prm = X + (int64_t)item_learner(item) * d.ld;
-  const int H = d.hidden, C = d.classes;
-  const int tid = threadIdx.x;
-  // thread: row tid / 4, units 4 (tid % 4) + 16 j, j = 0..3; every slice's
-  // loads are issued before the sums
-  const int r = tid >> 2, uq = 4 * (tid & 3);
-  if (r < rows) {
-    const int64_t at = ((int64_t)(r < 32 ? slot_a : slot_b) * kBatch + (r & 31)) * H + c0 + uq;
-    f32x4 p[kSkMaxSlices][4];
-#pragma unroll
-    for (int q = 0; q < kSkMaxSlices; ++q)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        p[q][j] = q < S ? *reinterpret_cast<const f32x4*>(Zpart + (int64_t)q * part_stride + at + 16 * j)
-                        : f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      f32x4 z = p[0][j];
-#pragma unroll
-      for (int q = 1; q < kSkMaxSlices; ++q)
-        if (q < S) z += p[q][j];
-      const f32x4 b = *reinterpret_cast<const f32x4*>(prm + d.off_b1 + c0 + uq + 16 * j);
-      z += b;
-      *reinterpret_cast<f32x4*>(Z1 + at + 16 * j) = z;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) Hs[r * kLdh + uq + 16 * j + t] = bf16r(fmaxf(z[t], 0.0f));
-    }
-  }
-  for (int k = tid; k < 64 * C; k += 256) W2s[k] = bf16r(prm[d.off_w2 + (int64_t)c0 * C + k]);
-  __syncthreads();
-  for (int o = tid; o < rows * C; o += 256) {
-    const int r = o / C, c = o % C;
-    float s = 0.0f;
-    for (int h = 0; h < 64; ++h) s += Hs[r * kLdh + h] * W2s[h * C + c];
-    Zp[(int64_t)(c0 / 64) * zp_stride +
-       ((int64_t)(r < 32 ? slot_a : slot_b) * kBatch + (r & 31)) * kMaxClasses + c] = s;
-  }
-}
-
-// Per mini-batch (blockIdx.x) and 64 hidden units (blockIdx.y): the logits
-// (shares summed in unit-block order, + b2), softmax cross-entropy and dZ2 =
-// (softmax - onehot) / 32 (recomputed by every unit block: 32 x classes
-// values).  Unit block 0 writes the loss and, when BACKWARD, db2 and the
-// padding of G.  When BACKWARD, wave w takes the 16 units c0 + 16w .. on
-// the matrix cores: dZ1 = (bf16(dZ2) bf16(W2)^T) * [Z1 > 0] (K = classes,
-// zero-padded to 32), stored in bf16 as [slot][unit][row] for k_mlp_wgrad,
-// db1 = its sum over the rows, and dW2 = bf16(relu(Z1))^T bf16(dZ2) (K = the
-// 32 rows).
+// Per mini-batch (blockIdx.x), all hidden units, 512 threads: Z1 = the S
+// partial slices summed in slice order + b1 (kept in LDS); the logits =
+// bf16(relu(Z1)) bf16(W2) + b2 on the matrix cores (classes zero-padded to
+// 16; each wave takes every eighth 32-unit K step and the waves' partial sums
+// are added in wave order); softmax cross-entropy, the loss and dZ2 =
+// (softmax - onehot) / 32.  When BACKWARD, wave w takes the unit tiles
+// 16 (w + 8 k) .. +15 on the matrix cores: dZ1 = (bf16(dZ2) bf16(W2)^T) *
+// [Z1 > 0] (K = classes, zero-padded to 32), stored in bf16 as
+// [slot][unit][row] for k_mlp_wgrad, db1 = its sum over the rows, and dW2 =
+// bf16(relu(Z1))^T bf16(dZ2) (K = the 32 rows); then db2 and the padding of G.
 template <bool BACKWARD>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(512)
     k_mlp_head(const float* __restrict__ X, const int32_t* __restrict__ ylab,
-               const float* __restrict__ Z1, const float* __restrict__ Zp, int64_t zp_stride,
-               __bf16* __restrict__ dZ1t, float* __restrict__ G, float* __restrict__ losses, Dims d,
-               List L) {
-  constexpr int kLdz = 64 + 1;
+                const float* __restrict__ Zpart, int64_t part_stride, int S,
+                __bf16* __restrict__ dZ1t, float* __restrict__ G, float* __restrict__ losses, Dims d,
+                List L) {
+  constexpr int kLdz = kMaxHidden + 4;
+  __shared__ __attribute__((aligned(16))) float Z1s[kBatch * kLdz];  // Z1 [row][unit]
+  __shared__ float W2s[kMaxHidden * kMaxClasses];                     // bf16(W2), [unit][class]
   __shared__ float Zs[kBatch * kMaxClasses];  // logits, then dZ2
   __shared__ float Zb[kBatch * kMaxClasses];  // bf16(dZ2), zero beyond the classes
-  __shared__ float W2s[64 * kMaxClasses];     // bf16(W2) of this block's units
-  __shared__ float Z1s[kBatch * kLdz];        // Z1 of this block's units
   __shared__ float row_loss[kBatch];
   __shared__ int ys[kBatch];
+  __shared__ float Lp[8 * kBatch * 16];  // each wave's partial logits
   const uint32_t item = L.w[blockIdx.x];
-  const int slot = item_slot_a(item);
+  const int slot = item_slot(item);
   const float* prm = X + (int64_t)item_learner(item) * d.ld;
   const int H = d.hidden, C = d.classes;
   const int blocks = H / 64;
-  const int c0 = blockIdx.y * 64;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t row0 = (int64_t)slot * kBatch;
 
-  // every load of this phase is independent of the others
-  for (int o = tid; o < kBatch * C; o += 256) {
-    const int r = o / C, c = o % C;
-    float z = 0.0f;
-    for (int q = 0; q < blocks; ++q) z += Zp[(int64_t)q * zp_stride + (row0 + r) * kMaxClasses + c];
-    Zs[r * kMaxClasses + c] = z + prm[d.off_b2 + c];
-  }
-  if (tid < kBatch) ys[tid] = ylab[row0 + tid];
-  if (BACKWARD) {
-    for (int k = tid; k < 64 * C; k += 256) W2s[k] = bf16r(prm[d.off_w2 + (int64_t)c0 * C + k]);
+  // Z1: thread takes row tid / 16 and units 4 (tid % 16) + 64 j
+  {
+    const int r = tid >> 4, uq = 4 * (tid & 15);
+    const float* src = Zpart + (row0 + r) * H + uq;
+    for (int j0 = 0; j0 < blocks; j0 += 4) {
+      f32x4 p[kSkMaxSlices][4];
 #pragma unroll
-    for (int u = 0; u < kBatch * 64 / 256; ++u) {
-      const int o = tid + 256 * u, r = o >> 6, h = o & 63;
-      Z1s[r * kLdz + h] = Z1[(row0 + r) * H + c0 + h];
+      for (int q = 0; q < kSkMaxSlices; ++q)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          p[q][j] = (q < S && j0 + j < blocks)
+                        ? *reinterpret_cast<const f32x4*>(src + (int64_t)q * part_stride + 64 * (j0 + j))
+                        : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (j0 + j >= blocks) break;
+        const int u = uq + 64 * (j0 + j);
+        f32x4 z = p[0][j];
+#pragma unroll
+        for (int q = 1; q < kSkMaxSlices; ++q)
+          if (q < S) z += p[q][j];
+        z += *reinterpret_cast<const f32x4*>(prm + d.off_b1 + u);
+        *reinterpret_cast<f32x4*>(Z1s + r * kLdz + u) = z;
+      }
     }
+  }
+  for (int k = tid; k < H * C; k += 512) W2s[k] = bf16r(prm[d.off_w2 + k]);
+  if (tid < kBatch) ys[tid] = ylab[row0 + tid];
+  __syncthreads();
+  // logits = bf16(relu(Z1)) bf16(W2) on the matrix cores: wave w takes the
+  // 32-unit K steps w, w + 8, .. for both 16-row tiles; the waves' partial
+  // sums are added in wave order
+  {
+    const int kq8 = 8 * (lane >> 4), cl = lane & 15;
+    f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    for (int ks = wave; ks < H / 32; ks += 8) {
+      const int u0 = 32 * ks + kq8;
+      bf16x8 fb;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) fb[t] = (__bf16)(cl < C ? W2s[(u0 + t) * C + cl] : 0.0f);
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        const float* z = Z1s + (16 * rt + cl) * kLdz + u0;
+        bf16x8 fa;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) fa[t] = (__bf16)fmaxf(z[t], 0.0f);
+        acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa, fb, acc[rt], 0, 0, 0);
+      }
+    }
+    // lane holds rows 16 rt + 4 (lane / 16) + t of class cl
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        Lp[(wave * kBatch + 16 * rt + 4 * (lane >> 4) + t) * 16 + cl] = acc[rt][t];
+  }
+  __syncthreads();
+  if (tid < kBatch * C) {
+    const int r = tid / C, c = tid % C;
+    float z = 0.0f;
+    for (int w = 0; w < 8; ++w) z += Lp[(w * kBatch + r) * 16 + c];
+    Zs[r * kMaxClasses + c] = z + prm[d.off_b2 + c];
   }
   __syncthreads();
   if (tid < kBatch) {
@@ -398,53 +369,52 @@ __global__ void __launch_bounds__(256)
   }
   __syncthreads();
   float* g = G + (int64_t)slot * d.ld;
-  if (blockIdx.y == 0) {
-    if (tid == 0) {
-      float s = 0.0f;
-      for (int r = 0; r < kBatch; ++r) s += row_loss[r];
-      losses[slot] = s * (1.0f / kBatch);
-    }
-    if (BACKWARD) {
-      if (tid < C) {
-        float s = 0.0f;
-        for (int r = 0; r < kBatch; ++r) s += Zs[r * kMaxClasses + tid];
-        g[d.off_b2 + tid] = s;
-      }
-      if (tid < d.P - d.off_pad) g[d.off_pad + tid] = 0.0f;
-    }
+  if (tid == 0) {
+    float s = 0.0f;
+    for (int r = 0; r < kBatch; ++r) s += row_loss[r];
+    losses[slot] = s * (1.0f / kBatch);
   }
   if (!BACKWARD) return;
-  const int hl = 16 * wave + (lane & 15);  // this lane's unit within the block
-  const int kq = 8 * (lane >> 4);          // this lane's K offset in a fragment
-  // dZ1 for rows 16 rt .. +15 and units 16w .. +15
-  bf16x8 fw;  // B[k][h] = bf16(W2[h][k]), k = class
-#pragma unroll
-  for (int t = 0; t < 8; ++t) fw[t] = (__bf16)(kq + t < C ? W2s[hl * C + kq + t] : 0.0f);
-  float db1 = 0.0f;
-#pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    bf16x8 fz;  // A[r][k] = bf16(dZ2[r][k])
-#pragma unroll
-    for (int t = 0; t < 8; ++t) fz[t] = (__bf16)(kq + t < kMaxClasses ? Zb[(16 * rt + (lane & 15)) * kMaxClasses + kq + t] : 0.0f);
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fz, fw, acc, 0, 0, 0);
-    // lane holds rows 16 rt + 4 (lane / 16) + t of unit hl
-    const int r0 = 16 * rt + 4 * (lane >> 4);
-    float v[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      v[t] = Z1s[(r0 + t) * kLdz + hl] > 0.0f ? acc[t] : 0.0f;
-      db1 += v[t];
-    }
-    const uint2 packed = {pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
-    *reinterpret_cast<uint2*>(dZ1t + ((int64_t)slot * H + c0 + hl) * kBatch + r0) = packed;
+  if (tid < C) {
+    float s = 0.0f;
+    for (int r = 0; r < kBatch; ++r) s += Zs[r * kMaxClasses + tid];
+    g[d.off_b2 + tid] = s;
   }
-  // db1: the four row groups of a unit sit in lanes l, l+16, l+32, l+48
-  db1 += __shfl_xor(db1, 16);
-  db1 += __shfl_xor(db1, 32);
-  if (lane < 16) g[d.off_b1 + c0 + hl] = db1;
-  // dW2[h][c] for units 16w .. +15: A[h][r] = bf16(relu(Z1[r][h])), B[r][c] = bf16(dZ2[r][c])
-  {
+  if (tid < d.P - d.off_pad) g[d.off_pad + tid] = 0.0f;
+  const int kq = 8 * (lane >> 4);  // this lane's K offset in a fragment
+  bf16x8 fz[2];                    // A[r][k] = bf16(dZ2[r][k]), row tiles 0 and 1
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      fz[rt][t] = (__bf16)(kq + t < kMaxClasses ? Zb[(16 * rt + (lane & 15)) * kMaxClasses + kq + t] : 0.0f);
+  for (int ut = wave; ut < H / 16; ut += 8) {
+    const int hl = 16 * ut + (lane & 15);  // this lane's unit
+    // dZ1 for rows 16 rt .. +15 and units 16 ut .. +15
+    bf16x8 fw;  // B[k][h] = bf16(W2[h][k]), k = class
+#pragma unroll
+    for (int t = 0; t < 8; ++t) fw[t] = (__bf16)(kq + t < C ? W2s[hl * C + kq + t] : 0.0f);
+    float db1 = 0.0f;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fz[rt], fw, acc, 0, 0, 0);
+      // lane holds rows 16 rt + 4 (lane / 16) + t of unit hl
+      const int r0 = 16 * rt + 4 * (lane >> 4);
+      float v[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        v[t] = Z1s[(r0 + t) * kLdz + hl] > 0.0f ? acc[t] : 0.0f;
+        db1 += v[t];
+      }
+      const uint2 packed = {pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+      *reinterpret_cast<uint2*>(dZ1t + ((int64_t)slot * H + hl) * kBatch + r0) = packed;
+    }
+    // db1: the four row groups of a unit sit in lanes l, l+16, l+32, l+48
+    db1 += __shfl_xor(db1, 16);
+    db1 += __shfl_xor(db1, 32);
+    if (lane < 16) g[d.off_b1 + hl] = db1;
+    // dW2[h][c] for units 16 ut .. +15: A[h][r] = bf16(relu(Z1[r][h])), B[r][c] = bf16(dZ2[r][c])
     bf16x8 fh, fd;
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
@@ -457,7 +427,7 @@ __global__ void __launch_bounds__(256)
     if (c < C) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const int h = c0 + 16 * wave + 4 * (lane >> 4) + t;
+        const int h = 16 * ut + 4 * (lane >> 4) + t;
         g[d.off_w2 + (int64_t)h * C + c] = acc[t];
       }
     }
@@ -477,7 +447,7 @@ __global__ void __launch_bounds__(256)
                 const __bf16* __restrict__ dZ1t, float* __restrict__ G, Dims d, List L) {
   constexpr int kLda = kBatch + 8;  // bf16 per transposed sample column (16-byte aligned)
   __shared__ __attribute__((aligned(16))) __bf16 At[kFeatBlock * kLda];
-  const int slot = item_slot_a(L.w[blockIdx.x]);
+  const int slot = item_slot(L.w[blockIdx.x]);
   const int f0 = blockIdx.y * kFeatBlock;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int H = d.hidden;
@@ -557,22 +527,16 @@ nbsgd_status check_shape(const nbsgd_mlp_shape* s, Dims* d) {
 
 size_t up256(size_t b) { return (b + 255) & ~(size_t)255; }
 
-// sample list, labels, Z1 [rows][hidden] fp32, hidden/64 logit-share planes
-// [rows][16] fp32, dZ1 [rows/32][hidden][32] bf16 and kSkMaxSlices partial Z1
-// planes [rows][hidden] fp32, each 256-byte aligned
+// sample list, labels, dZ1 [rows/32][hidden][32] bf16 and kSkMaxSlices partial
+// Z1 planes [rows][hidden] fp32, each 256-byte aligned
 size_t workspace_for(const Dims& d, int64_t rows) {
-  return 2 * up256((size_t)rows * 4) + up256((size_t)rows * d.hidden * 4) +
-         (size_t)(d.hidden / 64) * up256((size_t)rows * kMaxClasses * 4) +
-         up256((size_t)rows * d.hidden * 2) +
+  return 2 * up256((size_t)rows * 4) + up256((size_t)rows * d.hidden * 2) +
          (size_t)kSkMaxSlices * up256((size_t)rows * d.hidden * 4);
 }
 
 struct Workspace {
   int32_t* idx;
   int32_t* ylab;
-  float* z1;
-  float* zp;
-  int64_t zp_stride;  // floats between logit-share planes
   __bf16* dz1t;
   float* part;        // partial Z1 of each d_in slice
   int64_t part_stride;
@@ -585,11 +549,6 @@ Workspace carve(void* ws, const Dims& d, int64_t rows) {
   p += up256((size_t)rows * 4);
   w.ylab = reinterpret_cast<int32_t*>(p);
   p += up256((size_t)rows * 4);
-  w.z1 = reinterpret_cast<float*>(p);
-  p += up256((size_t)rows * d.hidden * 4);
-  w.zp = reinterpret_cast<float*>(p);
-  w.zp_stride = (int64_t)(up256((size_t)rows * kMaxClasses * 4) / 4);
-  p += (size_t)(d.hidden / 64) * up256((size_t)rows * kMaxClasses * 4);
   w.dz1t = reinterpret_cast<__bf16*>(p);
   p += up256((size_t)rows * d.hidden * 2);
   w.part = reinterpret_cast<float*>(p);
@@ -638,44 +597,17 @@ nbsgd_status launch_err(const char* what) {
 
 int item_learner_h(uint32_t w) { return (int)(w >> 24); }
 
-uint32_t item(int learner, int slot_a, int slot_b) {
-  return ((uint32_t)learner << 24) | ((uint32_t)slot_a << 12) | (uint32_t)(slot_b + 1);
-}
+uint32_t item(int learner, int slot) { return ((uint32_t)learner << 24) | ((uint32_t)slot << 12); }
 
 // Launches the three kernels over mini-batches `mb` (learner, slot), sorted
-// by learner, of one group (at most kMaxList): forward tiles pair
-// consecutive mini-batches of the same learner.
+// by learner, of one group (at most kMaxList).
 template <bool BACKWARD>
 void launch_group(const std::pair<int, int>* mb, int count, const float* X, const float* data,
                   const Workspace& w, float* G, float* losses, const Dims& d, hipStream_t st) {
-  const int nb = d.hidden / 64;
-  List tiles, items;
-  FwdMap M;
-  tiles.count = items.count = 0;
-  M.n = 0;
-  int total = 0;
-  for (int k = 0; k < count; ++k) {
-    if (k == 0 || mb[k].first != mb[k - 1].first) {  // a new learner
-      if (M.n > 0) total += nb * (tiles.count - M.first[M.n - 1]);
-      M.off[M.n] = total;
-      M.first[M.n] = tiles.count;
-      ++M.n;
-    }
-    items.w[items.count++] = item(mb[k].first, mb[k].second, -1);
-    if (k + 1 < count && mb[k + 1].first == mb[k].first) {
-      tiles.w[tiles.count++] = item(mb[k].first, mb[k].second, mb[k + 1].second);
-      ++k;
-      items.w[items.count++] = item(mb[k].first, mb[k].second, -1);
-    } else {
-      tiles.w[tiles.count++] = item(mb[k].first, mb[k].second, -1);
-    }
-  }
-  total += nb * (tiles.count - M.first[M.n - 1]);
-  M.off[M.n] = total;
-  M.first[M.n] = tiles.count;
-  for (int x = 0; x <= 8; ++x) M.xcd_start[x] = (int32_t)((int64_t)x * total / 8);
-  const int per_xcd = (total + 7) / 8;
-  // forward over quads of each learner's entries in `items`, then the slice sums
+  List items;
+  items.count = count;
+  for (int k = 0; k < count; ++k) items.w[k] = item(mb[k].first, mb[k].second);
+  // forward over quads of each learner's mini-batches, slices of d_in
   SkMap K;
   memset(&K, 0, sizeof K);
   const int chunks = d.d_in / kSkKc;
@@ -702,10 +634,8 @@ void launch_group(const std::pair<int, int>* mb, int count, const float* X, cons
   const int sk_per_xcd = (sk_total + 7) / 8;
   hipLaunchKernelGGL(k_mlp_fwd_sk, dim3(8 * sk_per_xcd), dim3(512), 0, st, X, data, w.idx, w.part,
                      w.part_stride, d, K, items);
-  hipLaunchKernelGGL(k_mlp_fwd_sum, dim3(8 * per_xcd), dim3(256), 0, st, X, w.part, w.part_stride,
-                     K.S, w.z1, w.zp, w.zp_stride, d, M, tiles);
-  hipLaunchKernelGGL(k_mlp_head<BACKWARD>, dim3(items.count, BACKWARD ? nb : 1), dim3(256), 0, st, X,
-                     w.ylab, w.z1, w.zp, w.zp_stride, w.dz1t, G, losses, d, items);
+  hipLaunchKernelGGL(k_mlp_head<BACKWARD>, dim3(items.count), dim3(512), 0, st, X, w.ylab, w.part,
+                     w.part_stride, K.S, w.dz1t, G, losses, d, items);
   if (BACKWARD)
     hipLaunchKernelGGL(k_mlp_wgrad, dim3(items.count, d.d_in / kFeatBlock), dim3(256), 0, st, data,
                        w.idx, w.dz1t, G, d, items);
