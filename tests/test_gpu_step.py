@@ -275,6 +275,52 @@ def test_tiny_workload_every_step():
             assert rel_err(r.X.cpu().numpy(), Xo) <= TOL, k
 
 
+def test_tiny_workload_graph_replays_match_eager():
+    """The 4-learner workload's iterations captured in a HIP graph (the step
+    makes no allocation, copy, memset or synchronisation, and carries its
+    per-step constants in the kernel arguments): every replay, from the same
+    starting replicas, equals the eager run bitwise, with eager work and
+    synchronisations between the replays; and the eager run is the oracle's."""
+    wl = workloads.TINY
+    _say("tiny workload graph capture and replays")
+    r = runner.StepRunner(wl, DEV)
+    X0, V0 = r.Xrows.clone(), r.Vrows.clone()
+    plans = [r.plan(k) for k in range(wl.steps)]
+    for mask, _, _, W in plans:
+        r.launch(mask, W)
+    torch.cuda.synchronize()
+    Xe, Ve = r.Xrows.clone(), r.Vrows.clone()
+    X0c, G = window_inputs(wl, np.arange(wl.P))
+    Xo, Vo = X0c.astype(np.float64), np.zeros((wl.n, wl.P))
+    mixer, d = OracleMixer(wl), oracle_delay(wl)
+    for k in range(wl.steps):
+        s = oracle.schedule.sample_schedule(wl.seed, k, wl.n, wl.m, d)
+        Xo, Vo = oracle.step.step(Xo, Vo, G, s["mask"], mixer.w(k), float(np.float32(wl.lr)),
+                                  float(np.float32(wl.momentum)), ORACLE_ORDER[wl.order])
+    assert rel_err(Xe[:, :wl.P].cpu().numpy(), Xo) <= TOL
+    assert rel_err(Ve[:, :wl.P].cpu().numpy(), Vo) <= TOL
+
+    r.Xrows.copy_(X0)
+    r.Vrows.copy_(V0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for mask, _, _, W in plans:
+            r.launch(mask, W)
+    for rep in range(3):
+        r.Xrows.copy_(X0)
+        r.Vrows.copy_(V0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(r.Xrows, Xe) and torch.equal(r.Vrows, Ve), rep
+        # eager work between replays: one more eager step on scratch copies
+        Xs, Vs = r.Xrows.clone(), r.Vrows.clone()
+        _lib.step_strided(Xs, Vs, r.Grows, wl.P, plans[0][0], plans[0][3], wl.lr, wl.momentum,
+                          r.order)
+        torch.cuda.synchronize()
+
+
 def _windows(P, seed, k=16, width=4096, edge=65536):
     rng = np.random.default_rng(seed)
     cols = [np.arange(0, min(edge, P)), np.arange(max(0, P - edge), P)]
