@@ -43,6 +43,7 @@ constexpr int kMaxClasses = 16;  // classes fill one 16-wide MFMA tile
 constexpr int kMaxList = 896;    // mini-batches per launch (kernel-argument list)
 constexpr int kMaxEval = 512;    // batches of 32 per nbsgd_mlp_loss call
 constexpr int kFeatBlock = 128;  // d_in features per k_mlp_wgrad workgroup
+constexpr int kHeadThreads = 1024;  // 16 waves per mini-batch in k_mlp_head
 
 struct Dims {
   int32_t d_in, hidden, classes;
@@ -255,22 +256,22 @@ __global__ void __launch_bounds__(512)
   }
 }
 
-// Per mini-batch (blockIdx.x), all hidden units, 512 threads: Z1 = the S
+// Per mini-batch (blockIdx.x), all hidden units, 16 waves: Z1 = the S
 // partial slices summed in slice order + b1 (kept in LDS); the logits =
 // bf16(relu(Z1)) bf16(W2) + b2 on the matrix cores (classes zero-padded to
-// 16; each wave takes every eighth 32-unit K step and the waves' partial sums
-// are added in wave order); softmax cross-entropy, the loss and dZ2 =
+// 16; each wave takes every sixteenth 32-unit K step and the waves' partial
+// sums are added in wave order); softmax cross-entropy, the loss and dZ2 =
 // (softmax - onehot) / 32.  When BACKWARD, wave w takes the unit tiles
-// 16 (w + 8 k) .. +15 on the matrix cores: dZ1 = (bf16(dZ2) bf16(W2)^T) *
+// 16 (w + 16 k) .. +15 on the matrix cores: dZ1 = (bf16(dZ2) bf16(W2)^T) *
 // [Z1 > 0] (K = classes, zero-padded to 32), stored in bf16 as
 // [slot][unit][row] for k_mlp_wgrad, db1 = its sum over the rows, and dW2 =
 // bf16(relu(Z1))^T bf16(dZ2) (K = the 32 rows); then db2 and the padding of G.
 template <bool BACKWARD>
-__global__ void __launch_bounds__(512)
+__global__ void __launch_bounds__(kHeadThreads)
     k_mlp_head(const float* __restrict__ X, const int32_t* __restrict__ ylab,
-                const float* __restrict__ Zpart, int64_t part_stride, int S,
-                __bf16* __restrict__ dZ1t, float* __restrict__ G, float* __restrict__ losses, Dims d,
-                List L) {
+               const float* __restrict__ Zpart, int64_t part_stride, int S,
+               __bf16* __restrict__ dZ1t, float* __restrict__ G, float* __restrict__ losses, Dims d,
+               List L) {
   constexpr int kLdz = kMaxHidden + 4;
   __shared__ __attribute__((aligned(16))) float Z1s[kBatch * kLdz];  // Z1 [row][unit]
   __shared__ float W2s[kMaxHidden * kMaxClasses];                     // bf16(W2), [unit][class]
@@ -278,32 +279,32 @@ __global__ void __launch_bounds__(512)
   __shared__ float Zb[kBatch * kMaxClasses];  // bf16(dZ2), zero beyond the classes
   __shared__ float row_loss[kBatch];
   __shared__ int ys[kBatch];
-  __shared__ float Lp[8 * kBatch * 16];  // each wave's partial logits
+  __shared__ float Lp[(kHeadThreads / 64) * kBatch * 16];  // each wave's partial logits
   const uint32_t item = L.w[blockIdx.x];
   const int slot = item_slot(item);
   const float* prm = X + (int64_t)item_learner(item) * d.ld;
   const int H = d.hidden, C = d.classes;
-  const int blocks = H / 64;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t row0 = (int64_t)slot * kBatch;
 
-  // Z1: thread takes row tid / 16 and units 4 (tid % 16) + 64 j
+  // Z1: thread takes row tid / TPR and units 4 (tid % TPR) + SPAN j
+  constexpr int TPR = kHeadThreads / 32, SPAN = 4 * TPR;
   {
-    const int r = tid >> 4, uq = 4 * (tid & 15);
+    const int r = tid / TPR, uq = 4 * (tid % TPR);
     const float* src = Zpart + (row0 + r) * H + uq;
-    for (int j0 = 0; j0 < blocks; j0 += 4) {
+    for (int j0 = 0; j0 * SPAN < H; j0 += 4) {
       f32x4 p[kSkMaxSlices][4];
 #pragma unroll
       for (int q = 0; q < kSkMaxSlices; ++q)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          p[q][j] = (q < S && j0 + j < blocks)
-                        ? *reinterpret_cast<const f32x4*>(src + (int64_t)q * part_stride + 64 * (j0 + j))
+          p[q][j] = (q < S && uq + SPAN * (j0 + j) < H)
+                        ? *reinterpret_cast<const f32x4*>(src + (int64_t)q * part_stride + SPAN * (j0 + j))
                         : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        if (j0 + j >= blocks) break;
-        const int u = uq + 64 * (j0 + j);
+        if (uq + SPAN * (j0 + j) >= H) break;
+        const int u = uq + SPAN * (j0 + j);
         f32x4 z = p[0][j];
 #pragma unroll
         for (int q = 1; q < kSkMaxSlices; ++q)
@@ -313,16 +314,16 @@ __global__ void __launch_bounds__(512)
       }
     }
   }
-  for (int k = tid; k < H * C; k += 512) W2s[k] = bf16r(prm[d.off_w2 + k]);
+  for (int k = tid; k < H * C; k += kHeadThreads) W2s[k] = bf16r(prm[d.off_w2 + k]);
   if (tid < kBatch) ys[tid] = ylab[row0 + tid];
   __syncthreads();
   // logits = bf16(relu(Z1)) bf16(W2) on the matrix cores: wave w takes the
-  // 32-unit K steps w, w + 8, .. for both 16-row tiles; the waves' partial
+  // 32-unit K steps w, w + 16, .. for both 16-row tiles; the waves' partial
   // sums are added in wave order
   {
     const int kq8 = 8 * (lane >> 4), cl = lane & 15;
     f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-    for (int ks = wave; ks < H / 32; ks += 8) {
+    for (int ks = wave; ks < H / 32; ks += kHeadThreads / 64) {
       const int u0 = 32 * ks + kq8;
       bf16x8 fb;
 #pragma unroll
@@ -347,7 +348,7 @@ __global__ void __launch_bounds__(512)
   if (tid < kBatch * C) {
     const int r = tid / C, c = tid % C;
     float z = 0.0f;
-    for (int w = 0; w < 8; ++w) z += Lp[(w * kBatch + r) * 16 + c];
+    for (int w = 0; w < kHeadThreads / 64; ++w) z += Lp[(w * kBatch + r) * 16 + c];
     Zs[r * kMaxClasses + c] = z + prm[d.off_b2 + c];
   }
   __syncthreads();
@@ -388,7 +389,7 @@ __global__ void __launch_bounds__(512)
 #pragma unroll
     for (int t = 0; t < 8; ++t)
       fz[rt][t] = (__bf16)(kq + t < kMaxClasses ? Zb[(16 * rt + (lane & 15)) * kMaxClasses + kq + t] : 0.0f);
-  for (int ut = wave; ut < H / 16; ut += 8) {
+  for (int ut = wave; ut < H / 16; ut += kHeadThreads / 64) {
     const int hl = 16 * ut + (lane & 15);  // this lane's unit
     // dZ1 for rows 16 rt .. +15 and units 16 ut .. +15
     bf16x8 fw;  // B[k][h] = bf16(W2[h][k]), k = class
@@ -634,7 +635,8 @@ void launch_group(const std::pair<int, int>* mb, int count, const float* X, cons
   const int sk_per_xcd = (sk_total + 7) / 8;
   hipLaunchKernelGGL(k_mlp_fwd_sk, dim3(8 * sk_per_xcd), dim3(512), 0, st, X, data, w.idx, w.part,
                      w.part_stride, d, K, items);
-  hipLaunchKernelGGL(k_mlp_head<BACKWARD>, dim3(items.count), dim3(512), 0, st, X, w.ylab, w.part,
+  hipLaunchKernelGGL(k_mlp_head<BACKWARD>, dim3(items.count), dim3(kHeadThreads), 0, st, X, w.ylab,
+                     w.part,
                      w.part_stride, K.S, w.dz1t, G, losses, d, items);
   if (BACKWARD)
     hipLaunchKernelGGL(k_mlp_wgrad, dim3(items.count, d.d_in / kFeatBlock), dim3(256), 0, st, data,
