@@ -68,6 +68,58 @@ def test_grad_small_shape_every_entry(tiny):
                 assert (G[i, j] == 7.0).all() and L[i, j] == -1.0
 
 
+@pytest.mark.parametrize("d_in,hidden,classes", [(384, 192, 10), (640, 320, 16), (256, 512, 2),
+                                                  (128, 64, 16)])
+def test_grad_and_loss_odd_shapes_every_entry(d_in, hidden, classes):
+    """Shapes whose d_in splits into 3 or 2 slices (d_in / 64 = 6 or 10) and
+    whose hidden units leave a half-filled 128-unit block (192, 320), two and
+    sixteen classes; three learners with 1-5 finished mini-batches each, so
+    the forward's 4-mini-batch groups come in every size; every finished
+    entry and the evaluation losses against the oracle."""
+    n, m, n_samples = 3, 5, 300
+    s = Shape(d_in, hidden, classes, 32)
+    A = mlp_data.inputs(7, n_samples, d_in)
+    y = mlp_data.teacher_labels(7, A, hidden, classes)
+    x0 = mlp_data.student_init(7, d_in, hidden, classes)
+    rng = np.random.default_rng(d_in + hidden + classes)
+    X = (x0[None, :] + 0.05 * rng.standard_normal((n, s.n_params))).astype(np.float32)
+    mask = np.zeros((n, m), np.uint8)
+    for i, c in enumerate((1, 5, 3)):
+        mask[i, rng.permutation(m)[:c]] = 1  # not a prefix
+    idx = rng.integers(0, n_samples, size=(n, m, 32)).astype(np.int32)
+    _say(f"mlp grad shape d_in={d_in} hidden={hidden} classes={classes}")
+    dims = (d_in, hidden, classes)
+    P = _lib.mlp_param_count(*dims)
+    Xd = torch.from_numpy(pad_cols(X, P)).to(DEV)
+    data = torch.from_numpy(A).to(DEV)
+    labels = torch.from_numpy(y.astype(np.int32)).to(DEV)
+    G = torch.full((n, m, P), 7.0, dtype=torch.float32, device=DEV)
+    losses = torch.full((n * m,), -1.0, dtype=torch.float32, device=DEV)
+    rows = max(n * m * 32, 160)
+    ws = torch.empty((_lib.mlp_workspace_bytes(*dims, rows) + 15) // 16 * 4, dtype=torch.float32,
+                     device=DEV)
+    _lib.mlp_grad(Xd, m, dims, data, labels, idx, mask, G, losses, ws)
+    ev_idx = rng.integers(0, n_samples, size=160).astype(np.int32)
+    ev = torch.full((5,), -1.0, dtype=torch.float32, device=DEV)
+    _lib.mlp_loss(Xd[2], dims, data, labels, ev_idx, ev, ws)
+    torch.cuda.synchronize()
+    Gh, Lh = G.cpu().numpy(), losses.cpu().numpy().reshape(n, m)
+    for i in range(n):
+        for j in range(m):
+            if mask[i, j]:
+                g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
+                assert rel_err_blocks(Gh[i, j], g, mlp_blocks(*dims)) <= TOL_BF16, (i, j)
+                assert (Gh[i, j, s.n_params:] == 0).all()
+                assert abs(Lh[i, j] - loss) <= TOL_BF16 * abs(loss)
+            else:
+                assert (Gh[i, j] == 7.0).all() and Lh[i, j] == -1.0
+    evh = ev.cpu().numpy()
+    for k in range(5):
+        b = ev_idx[32 * k:32 * k + 32]
+        _, loss = oracle.mlp.grad(X[2], A[b], y[b], s, BF16)
+        assert abs(evh[k] - loss) <= TOL_BF16 * abs(loss), k
+
+
 def test_grad_full_shape_sampled_entries():
     """The full shape in the runner's launch configuration: padded rows
     (row_stride(P) = 2^21 floats apart) through nbsgd_mlp_grad_strided."""
