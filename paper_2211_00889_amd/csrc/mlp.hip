@@ -76,7 +76,7 @@ static_assert(sizeof(List) + sizeof(Dims) + 10 * 8 <= 4096, "kernel arguments ex
 static_assert(sizeof(IdxChunk) + 32 <= 4096, "kernel arguments exceed 4 KiB");
 static_assert(kMaxList <= 4096 && kMaxEval <= 4096, "slots are packed in 16 bits");
 
-__device__ __forceinline__ int item_learner(uint32_t w) { return (int)(w >> 24); }
+__host__ __device__ __forceinline__ int item_learner(uint32_t w) { return (int)(w >> 24); }
 __device__ __forceinline__ int item_slot(uint32_t w) { return (int)((w >> 12) & 0xfffu); }
 
 __device__ __forceinline__ float bf16r(float x) { return (float)(__bf16)x; }
@@ -103,7 +103,6 @@ __global__ void __launch_bounds__(256)
   dst[slot * kBatch + r] = v;
   ylab[slot * kBatch + r] = y < 0 ? 0 : (y >= classes ? classes - 1 : y);
 }
-
 
 // Forward, split over d_in.  Work item: a quad (up to four mini-batches of one
 // learner, 128 rows), a block of 128 hidden units and one of S equal slices of
@@ -596,8 +595,6 @@ nbsgd_status launch_err(const char* what) {
   return NBSGD_OK;
 }
 
-int item_learner_h(uint32_t w) { return (int)(w >> 24); }
-
 uint32_t item(int learner, int slot) { return ((uint32_t)learner << 24) | ((uint32_t)slot << 12); }
 
 // Launches the three kernels over mini-batches `mb` (learner, slot), sorted
@@ -621,7 +618,7 @@ void launch_group(const std::pair<int, int>* mb, int count, const float* X, cons
   K.ub = (d.hidden + kSkUnits - 1) / kSkUnits;
   int sk_total = 0;
   for (int k = 0; k < items.count; ++k) {
-    if (k == 0 || item_learner_h(items.w[k]) != item_learner_h(items.w[k - 1])) {
+    if (k == 0 || item_learner(items.w[k]) != item_learner(items.w[k - 1])) {
       if (K.n > 0) sk_total += K.S * K.ub * ((k - K.first[K.n - 1] + 3) / 4);
       K.off[K.n] = sk_total;
       K.first[K.n] = k;
@@ -636,8 +633,7 @@ void launch_group(const std::pair<int, int>* mb, int count, const float* X, cons
   hipLaunchKernelGGL(k_mlp_fwd_sk, dim3(8 * sk_per_xcd), dim3(512), 0, st, X, data, w.idx, w.part,
                      w.part_stride, d, K, items);
   hipLaunchKernelGGL(k_mlp_head<BACKWARD>, dim3(items.count), dim3(kHeadThreads), 0, st, X, w.ylab,
-                     w.part,
-                     w.part_stride, K.S, w.dz1t, G, losses, d, items);
+                     w.part, w.part_stride, K.S, w.dz1t, G, losses, d, items);
   if (BACKWARD)
     hipLaunchKernelGGL(k_mlp_wgrad, dim3(items.count, d.d_in / kFeatBlock), dim3(256), 0, st, data,
                        w.idx, w.dz1t, G, d, items);
