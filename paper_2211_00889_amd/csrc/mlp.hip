@@ -440,8 +440,10 @@ __global__ void __launch_bounds__(kHeadThreads)
 // unit) is a 16-byte read of the [slot][unit][row] dZ1 copy, the B operand (8
 // rows of one feature) comes from the sample rows staged transposed in LDS,
 // and each lane's four results are consecutive units of one G row: one
-// 16-byte store.  Wave w takes unit tiles w, w+4, ...; a workgroup writes
-// 128 whole G rows of dW1.
+// 16-byte store.  Wave w takes the hidden/64 consecutive unit tiles from
+// w * hidden/64 and stores them feature tile by feature tile, so its
+// consecutive stores fill whole 128-byte lines; a workgroup writes 128 whole
+// G rows of dW1.
 __global__ void __launch_bounds__(256)
     k_mlp_wgrad(const float* __restrict__ data, const int32_t* __restrict__ idx,
                 const __bf16* __restrict__ dZ1t, float* __restrict__ G, Dims d, List L) {
@@ -452,14 +454,15 @@ __global__ void __launch_bounds__(256)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int H = d.hidden;
   const int64_t row0 = (int64_t)slot * kBatch;
-  // this wave's dZ1 fragments (unit tiles wave, wave+4, ... < H/16 <= 32),
+  // this wave's dZ1 fragments (hidden/64 <= 8 consecutive unit tiles),
   // loaded before the sample rows so both latencies overlap
   const __bf16* dz = dZ1t + row0 * H + 8 * (lane >> 4);  // [unit][row] of this mini-batch
   bf16x8 fa[kMaxHidden / 64];
+  const int per = H / 64;  // unit tiles of this wave: wave * per .. + per - 1
 #pragma unroll
   for (int u = 0; u < kMaxHidden / 64; ++u) {
-    const int ht = wave + 4 * u;
-    if (16 * ht < H) fa[u] = *reinterpret_cast<const bf16x8*>(dz + (int64_t)(16 * ht + (lane & 15)) * kBatch);
+    const int ht = wave * per + u;
+    if (u < per) fa[u] = *reinterpret_cast<const bf16x8*>(dz + (int64_t)(16 * ht + (lane & 15)) * kBatch);
   }
   {
     // rows 2p, 2p+1 (p = tid / 16) of the mini-batch, features 4q .. 4q+3 and
@@ -488,14 +491,13 @@ __global__ void __launch_bounds__(256)
         &At[(16 * ft + (lane & 15)) * kLda + 8 * ((lane >> 4) ^ (ft & 3))]);
   float* g = G + (int64_t)slot * d.ld + (int64_t)(f0 + (lane & 15)) * H + 4 * (lane >> 4);
 #pragma unroll
-  for (int u = 0; u < kMaxHidden / 64; ++u) {
-    const int ht = wave + 4 * u;
-    if (16 * ht >= H) break;
+  for (int ft = 0; ft < kFeatBlock / 16; ++ft) {
 #pragma unroll
-    for (int ft = 0; ft < kFeatBlock / 16; ++ft) {
+    for (int u = 0; u < kMaxHidden / 64; ++u) {
+      if (u >= per) break;
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[u], fb[ft], acc, 0, 0, 0);
-      *reinterpret_cast<f32x4*>(g + (int64_t)(16 * ft) * H + 16 * ht) = acc;
+      *reinterpret_cast<f32x4*>(g + (int64_t)(16 * ft) * H + 16 * (wave * per + u)) = acc;
     }
   }
 }
