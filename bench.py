@@ -121,20 +121,72 @@ def cpu_baseline(wl, budget_s: float = 15.0, cols: int = 1 << 19):
                       f"is constant)"}
 
 
+def cpu_baseline_mlp(wl, A, y, x0, budget_s: float = 15.0):
+    """The oracle's MLP iterations (schedule, the bf16-input gradient of every
+    finished mini-batch in fp64, the step), one thread, whole iterations until
+    ``budget_s`` has passed; returns finished training samples per second.
+    The oracle's evaluations of the average replica are not timed."""
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    from oracle.mlp import BF16, Shape
+
+    s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
+    n, m, P = wl.n, wl.m, s.n_params
+    kinds = {"const": oracle.schedule.DELAY_CONST, "exp": oracle.schedule.DELAY_EXP,
+             "lomax": oracle.schedule.DELAY_LOMAX}
+    d = oracle.schedule.Delay(kinds[wl.delay.kind], wl.delay.base, wl.delay.param,
+                              wl.delay.slow_learner, wl.delay.slow_factor, wl.delay.slow_prob)
+    W = oracle.mixing.w_ring(n).astype(np.float32).astype(np.float64)
+    order = (oracle.step.MIX_THEN_STEP if wl.order == "mix_then_step"
+             else oracle.step.STEP_THEN_MIX)
+    lr, mu = float(np.float32(wl.lr)), float(np.float32(wl.momentum))
+    shuf = oracle.mlp.Shuffler(wl.seed, wl.n_samples // n, m, wl.batch)
+    X = np.tile(np.asarray(x0, dtype=np.float64), (n, 1))
+    V = np.zeros_like(X)
+    G = np.zeros((n, m, P))
+    finished, k = 0, 0
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        while True:
+            sch = oracle.schedule.sample_schedule(wl.seed, k, n, m, d)
+            for i in range(n):
+                idx = shuf.indices(k, i)
+                for j in range(m):
+                    if sch["mask"][i, j]:
+                        G[i, j] = oracle.mlp.grad(X[i], A[idx[j]], y[idx[j]], s, BF16)[0]
+            X, V = oracle.step.step(X, V, G, sch["mask"], W, lr, mu, order)
+            finished += int(sch["mask"].sum())
+            k += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s:
+                break
+    return {"value": finished * wl.batch / el, "unit": "samples/s", "cores": 1, "kind": "oracle",
+            "sample": f"{wl.name}: iterations 0..{k - 1} ({finished} finished mini-batches) in "
+                      f"{el:.1f} s (fp64 NumPy with bf16-rounded GEMM inputs, 1 thread; "
+                      f"evaluations not timed)"}
+
+
 def bench_mlp(args):
     """End-to-end MLP workload: per iteration the schedule, the shuffled
     indices, the per-mini-batch gradients on the matrix cores and the fused
     step.  Prints one JSON line with finished training samples per second,
-    the algorithmic GEMM work and the device-time split between the gradient
-    kernels and the step; per-kernel times come from rocprofv3."""
+    the algorithmic GEMM work, the device-time split between the gradient
+    kernels and the step, the step's roofline figure and the oracle's rate on
+    the same workload; per-kernel times come from rocprofv3."""
     import torch
 
     from paper_2211_00889_amd import runner
     from synth import workloads
 
+    from synth import mlp_data
+
     wl = workloads.MLP
     dev = torch.device("cuda:0")
-    r = runner.MlpRunner(wl, dev)
+    A = mlp_data.inputs(wl.seed, wl.n_samples, wl.d_in)
+    y = mlp_data.teacher_labels(wl.seed, A, wl.hidden, wl.classes)
+    x0 = mlp_data.student_init(wl.seed, wl.d_in, wl.hidden, wl.classes)
+    r = runner.MlpRunner(wl, dev, A, y, x0)
     for k in range(args.warmup):
         r.step(k)
     torch.cuda.synchronize()
@@ -161,7 +213,8 @@ def bench_mlp(args):
     step_bytes = 4 * r.P * (split_finished / len(events) + 4 * wl.n)
     loss = float(r.evaluate().mean().cpu())
     gemm_flop = 2 * 2 * wl.batch * wl.d_in * wl.hidden * finished  # forward and dW1 GEMMs
-    print(json.dumps({
+    step_gbps = step_bytes / (step_ms * 1e-3) / 1e9
+    out = {
         "metric": "end-to-end MLP Non-blocking D-PSGD: finished training samples per second",
         "value": finished * wl.batch / wall, "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps, "higher_is_better": True,
@@ -170,10 +223,20 @@ def bench_mlp(args):
                    "P": wl.P, "row_stride": r.ld, "mean_finished_per_step": finished / args.steps},
         "layer1_gemm_tflop_per_step": gemm_flop / args.steps / 1e12,
         "split_ms": {"gradients": grad_ms, "step": step_ms, "iterations": len(events)},
-        "step_gbps": step_bytes / (step_ms * 1e-3) / 1e9,
+        "step_gbps": step_gbps,
         "gradient_tflops": split_flop / (grad_ms * 1e-3) / 1e12,
         "gradient_frac_of_bf16_dense_peak": split_flop / (grad_ms * 1e-3) / 2.5e15,
-        "eval_loss_after": loss}), flush=True)
+        "roofline": {"bound": "hbm", "achieved": step_gbps, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": step_gbps / PEAK_HBM_GBS, "traffic": None, "kernel": "k_step",
+                     "kernel_ms_mean": step_ms, "alg_bytes_per_launch_mean": step_bytes,
+                     "note": "the fused step, the iteration's largest kernel; events around it "
+                             "in the split pass"},
+        "eval_loss_after": loss}
+    del r
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_mlp(wl, A, y, x0, args.cpu_budget)
+    print(json.dumps(out), flush=True)
 
 
 def bench_graph(args, wl, r, dev):
