@@ -48,7 +48,6 @@ constexpr int kWaves = 4;
 constexpr int kBlock = kWave * kWaves;
 constexpr int kMaxN = NBSGD_MAX_LEARNERS;
 constexpr int kMaxM = NBSGD_MAX_MINIBATCHES;
-constexpr int kSlots = (kMaxN + kWaves - 1) / kWaves;  // learners per wave
 
 // fused step kernel shape
 constexpr int kStepWaves = 8;
@@ -56,6 +55,10 @@ constexpr int kStepBlock = kWave * kStepWaves;
 constexpr int kStepSlots = (kMaxN + kStepWaves - 1) / kStepWaves;
 constexpr int kMaxRows = kMaxN * kMaxM;           // finished rows of one step
 constexpr int kMaxRuns = kMaxN + kStepWaves - 1;  // partial-sum slots
+// the fused step's LDS: n rows of values to mix and one row per run, 64 lanes
+// of float4 each; within the 64 KiB a workgroup may allocate
+static_assert((kMaxN + kMaxRuns) * kWave * 4 * sizeof(float) <= 64 * 1024,
+              "fused step LDS exceeds 64 KiB");
 
 template <int VEC>
 struct Vec;
