@@ -13,7 +13,8 @@
 // 2 or 1), so each wave moves 64 * VEC * 4 contiguous bytes per row per load.
 //
 // Fused step, one workgroup = 8 waves x 64 lanes, one VEC-vector column per
-// lane, all n learners:
+// lane, all n learners; workgroups take the column tiles from the last to the
+// first (the order never changes a result: columns are independent):
 //   phase 1: the finished gradient rows of the tile (sum_i c_i of them, in
 //            learner-major order) are split into 8 equal contiguous segments,
 //            one per wave, so a straggler-skewed mask (one learner with all m
@@ -205,7 +206,10 @@ __global__ void __launch_bounds__(kStepBlock)
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int64_t v = (int64_t)blockIdx.x * kWave + lane;
+  // tiles in decreasing column order: gradient rows written just before in
+  // increasing column order (the MLP gradient kernels) are read newest first,
+  // while the memory-side cache may still hold them
+  const int64_t v = (int64_t)(gridDim.x - 1 - blockIdx.x) * kWave + lane;
   const bool live = v < pv;
 
   // phase 1: own learners' X and V, and this wave's share of the G rows
