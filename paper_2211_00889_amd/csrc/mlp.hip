@@ -40,7 +40,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kBatch = 32;       // mini-batch size (the MFMA K of dW1)
 constexpr int kMaxHidden = 512;
 constexpr int kMaxClasses = 16;  // classes fill one 16-wide MFMA tile
-constexpr int kMaxList = 896;    // mini-batches per launch (kernel-argument list)
+constexpr int kMaxList = 896;    // mini-batches per launch group (kernel-argument list)
 constexpr int kMaxEval = 512;    // batches of 32 per nbsgd_mlp_loss call
 constexpr int kFeatBlock = 128;  // d_in features per k_mlp_wgrad workgroup
 constexpr int kHeadThreads = 1024;  // 16 waves per mini-batch in k_mlp_head
@@ -52,26 +52,35 @@ struct Dims {
   int64_t off_b1, off_w2, off_b2, off_pad;
 };
 
-// One launch's mini-batches, word k = learner << 24 | slot << 12, sorted by
-// learner.  A slot indexes the sample list (slot * 32 ..), the workspace rows
-// and the loss output.  Read as 32-bit words only.
+// One launch group's mini-batches, word e = learner << 24 | slot << 12,
+// sorted by learner.  A slot indexes the caller's sample list (slot * 32 ..),
+// the G rows and the loss output; the workspace rows of entry e are
+// e * 32 .. e * 32 + 31.  Read as 32-bit words only.
 struct List {
   int32_t count;
   uint32_t w[kMaxList];
 };
 
-// Sample indices of up to kUpSlots mini-batches: word k of `slot` holds
-// slots 2k and 2k+1 (16 bits each); `v` holds 32 indices per slot, two to a
-// word (16 bits each) when `wide` is 0, one to a word otherwise.
+// Sample indices of list entries first .. first + n_slots - 1, 32 per entry:
+// two to a word (16 bits each) when `wide` is 0, one to a word otherwise.
 constexpr int kUpSlots = 60;
 struct IdxChunk {
-  int32_t n_slots, wide;
-  uint32_t slot[kUpSlots / 2];
+  int32_t first, n_slots, wide;
   uint32_t v[kUpSlots * kBatch / 2];
 };
 
-// kernel arguments are limited to 4 KiB: the list, the shapes, the forward
-// map and at most ten pointers or 64-bit scalars
+// Sample indices of a whole launch group carried in the forward kernel's
+// arguments (groups of at most kInline mini-batches whose indices all fit 16
+// bits): row e * 32 + r in the 16-bit half r % 2 of word (e * 32 + r) / 2.
+constexpr int kInline = 56;
+template <int N>
+struct Idx16 {
+  uint32_t v[N];
+};
+using InlineIdx = Idx16<kInline * kBatch / 2>;
+
+// kernel arguments are limited to 4 KiB: the list, the shapes and at most
+// ten pointers or 64-bit scalars
 static_assert(sizeof(List) + sizeof(Dims) + 10 * 8 <= 4096, "kernel arguments exceed 4 KiB");
 static_assert(sizeof(IdxChunk) + 32 <= 4096, "kernel arguments exceed 4 KiB");
 static_assert(kMaxList <= 4096 && kMaxEval <= 4096, "slots are packed in 16 bits");
@@ -89,19 +98,13 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return (uint32_t)ua | ((uint32_t)ub << 16);
 }
 
-// Writes the sample index and its label (clamped into [0, classes)) of every
-// row of the listed mini-batches.
-__global__ void __launch_bounds__(256)
-    k_put_idx(int32_t* __restrict__ dst, int32_t* __restrict__ ylab,
-              const int32_t* __restrict__ labels, int32_t classes, IdxChunk c) {
+// Writes the sample index of every row of the chunk's list entries (used
+// when a group's indices do not fit the forward kernel's arguments).
+__global__ void __launch_bounds__(256) k_put_idx(int32_t* __restrict__ dst, IdxChunk c) {
   const int t = blockIdx.x * 256 + threadIdx.x;
-  const int k = t >> 5, r = t & 31;
-  if (k >= c.n_slots) return;
-  const int slot = (int)((c.slot[k >> 1] >> (16 * (k & 1))) & 0xffffu);
+  if (t >= c.n_slots * kBatch) return;
   const int32_t v = c.wide ? (int32_t)c.v[t] : (int32_t)((c.v[t >> 1] >> (16 * (t & 1))) & 0xffffu);
-  const int32_t y = labels[v];
-  dst[slot * kBatch + r] = v;
-  ylab[slot * kBatch + r] = y < 0 ? 0 : (y >= classes ? classes - 1 : y);
+  dst[c.first * kBatch + t] = v;
 }
 
 // Forward, split over d_in.  Work item: a quad (up to four mini-batches of one
@@ -111,30 +114,37 @@ __global__ void __launch_bounds__(256)
 // 16-byte read is one MFMA fragment.  Eight waves: wave w takes rows
 // 32 (w % 4) .. +31 and units 64 (w / 4) .. +63 (2 x 4 accumulators).  The
 // partial sums go to slice s of the partial buffer; k_mlp_head adds the
-// slices in slice order.
+// slices in slice order.  The work items are split into eight equal ranges,
+// one per XCD (workgroup b runs on XCD b % 8), so the items of one learner
+// share an L2.  INLINE: the sample indices come from the kernel arguments and
+// the workgroups of slice 0 and unit block 0 copy them to the workspace for
+// the later kernels; otherwise they are read from the workspace.
 constexpr int kSkRows = 128, kSkUnits = 128, kSkKc = 64, kSkLd = kSkKc + 8;
 constexpr int kSkMaxSlices = 4;
 struct SkMap {
   int32_t n;              // learners present
   int32_t S;              // K slices
   int32_t ub;             // unit blocks
-  int32_t xcd_start[9];   // item range of each XCD
+  uint32_t learner[4];    // learner id of present learner k in byte k % 4 of word k / 4
   int32_t off[17];        // first work item of each learner (off[n] = total)
   int32_t first[17];      // first list entry of each learner (first[n] = count)
 };
-static_assert(sizeof(List) + sizeof(Dims) + sizeof(SkMap) + 5 * 8 <= 4096,
+static_assert(NBSGD_MAX_LEARNERS <= 16, "SkMap holds at most 16 learners");
+static_assert(sizeof(InlineIdx) + sizeof(Dims) + sizeof(SkMap) + 5 * 8 <= 4096,
               "kernel arguments exceed 4 KiB");
 
+template <bool INLINE>
 __global__ void __launch_bounds__(512)
     k_mlp_fwd_sk(const float* __restrict__ X, const float* __restrict__ data,
-                 const int32_t* __restrict__ idx, float* __restrict__ Zpart, int64_t part_stride,
-                 Dims d, SkMap M, List L) {
+                 int32_t* __restrict__ idx, float* __restrict__ Zpart, int64_t part_stride, Dims d,
+                 SkMap M, Idx16<INLINE ? kInline * kBatch / 2 : 1> I) {
   constexpr int kDepth = 2;  // chunks loaded ahead of the one being staged
   __shared__ __attribute__((aligned(16))) __bf16 As[2][kSkRows * kSkLd];
   __shared__ __attribute__((aligned(16))) __bf16 Ws[2][kSkUnits * kSkLd];
   const int xcd = blockIdx.x & 7;
-  const int g = M.xcd_start[xcd] + (int)(blockIdx.x >> 3);
-  if (g >= M.xcd_start[xcd + 1]) return;  // uniform
+  const int64_t total = M.off[M.n];
+  const int g = (int)(xcd * total / 8) + (int)(blockIdx.x >> 3);
+  if (g >= (int)((xcd + 1) * total / 8)) return;  // uniform
   int li = 0;
   while (li + 1 < M.n && M.off[li + 1] <= g) ++li;
   const int cnt = M.first[li + 1] - M.first[li];
@@ -151,7 +161,8 @@ __global__ void __launch_bounds__(512)
   const int units = min(kSkUnits, H - u0);
   const int kslice = d.d_in / M.S, nck = kslice / kSkKc;
   const int kb = s * kslice;
-  const float* prm = X + (int64_t)item_learner(L.w[e0]) * d.ld;
+  const int learner = (int)((M.learner[li >> 2] >> (8 * (li & 3))) & 0xffu);
+  const float* prm = X + (int64_t)learner * d.ld;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave & 3, wu = wave >> 2;
   const bool mma = 32 * wr < rows && 64 * wu < units;  // wave-uniform
@@ -161,8 +172,15 @@ __global__ void __launch_bounds__(512)
   const bool alive = arow < rows;
   const float* asrc = data;
   if (alive) {
-    const int slot = item_slot(L.w[e0 + (arow >> 5)]);
-    asrc = data + (int64_t)idx[slot * kBatch + (arow & 31)] * d.d_in + kb + 4 * aq;
+    const int t = e0 * kBatch + arow;  // workspace row: entry e0 + arow / 32, row arow % 32
+    int32_t v;
+    if constexpr (INLINE) {
+      v = (int32_t)((I.v[t >> 1] >> (16 * (t & 1))) & 0xffffu);
+      if (s == 0 && ubk == 0 && aq == 0) idx[t] = v;
+    } else {
+      v = idx[t];
+    }
+    asrc = data + (int64_t)v * d.d_in + kb + 4 * aq;
   }
   // W1 staging: k rows 4 wa .. +3, units 4 wq .. +3
   const int wa = tid >> 5, wq = tid & 31;
@@ -247,15 +265,16 @@ __global__ void __launch_bounds__(512)
     for (int t = 0; t < 4; ++t) {
       const int r = 32 * wr + 16 * f + 4 * (lane >> 4) + t;
       if (r >= rows) continue;
-      const int slot = item_slot(L.w[e0 + (r >> 5)]);
-      float* o = out + ((int64_t)slot * kBatch + (r & 31)) * H + u0 + 64 * wu + (lane & 15);
+      float* o = out + ((int64_t)e0 * kBatch + r) * H + u0 + 64 * wu + (lane & 15);
 #pragma unroll
       for (int u = 0; u < 4; ++u) o[16 * u] = acc[f][u][t];
     }
   }
 }
 
-// Per mini-batch (blockIdx.x), all hidden units, 16 waves: Z1 = the S
+// Per list entry e = blockIdx.x (workspace rows e * 32 ..; G row and loss of
+// its slot), all hidden units, 16 waves: the rows' labels (clamped into
+// [0, classes)); Z1 = the S
 // partial slices summed in slice order + b1 (kept in LDS); the logits =
 // bf16(relu(Z1)) bf16(W2) + b2 on the matrix cores (classes zero-padded to
 // 16; each wave takes every sixteenth 32-unit K step and the waves' partial
@@ -263,12 +282,13 @@ __global__ void __launch_bounds__(512)
 // (softmax - onehot) / 32.  When BACKWARD, wave w takes the unit tiles
 // 16 (w + 16 k) .. +15 on the matrix cores: dZ1 = (bf16(dZ2) bf16(W2)^T) *
 // [Z1 > 0] (K = classes, zero-padded to 32), stored in bf16 as
-// [slot][unit][row] for k_mlp_wgrad, db1 = its sum over the rows, and dW2 =
+// [entry][unit][row] for k_mlp_wgrad, db1 = its sum over the rows, and dW2 =
 // bf16(relu(Z1))^T bf16(dZ2) (K = the 32 rows); then db2 and the padding of G.
 template <bool BACKWARD>
 __global__ void __launch_bounds__(kHeadThreads)
-    k_mlp_head(const float* __restrict__ X, const int32_t* __restrict__ ylab,
-               const float* __restrict__ Zpart, int64_t part_stride, int S,
+    k_mlp_head(const float* __restrict__ X, const int32_t* __restrict__ idx,
+               const int32_t* __restrict__ labels, const float* __restrict__ Zpart,
+               int64_t part_stride, int S,
                __bf16* __restrict__ dZ1t, float* __restrict__ G, float* __restrict__ losses, Dims d,
                List L) {
   constexpr int kLdz = kMaxHidden + 4;
@@ -284,7 +304,8 @@ __global__ void __launch_bounds__(kHeadThreads)
   const float* prm = X + (int64_t)item_learner(item) * d.ld;
   const int H = d.hidden, C = d.classes;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t row0 = (int64_t)slot * kBatch;
+  const int64_t row0 = (int64_t)blockIdx.x * kBatch;
+  const int32_t sample = tid < kBatch ? idx[row0 + tid] : 0;  // loaded ahead of its use
 
   // Z1: thread takes row tid / TPR and units 4 (tid % TPR) + SPAN j
   constexpr int TPR = kHeadThreads / 32, SPAN = 4 * TPR;
@@ -314,7 +335,10 @@ __global__ void __launch_bounds__(kHeadThreads)
     }
   }
   for (int k = tid; k < H * C; k += kHeadThreads) W2s[k] = bf16r(prm[d.off_w2 + k]);
-  if (tid < kBatch) ys[tid] = ylab[row0 + tid];
+  if (tid < kBatch) {
+    const int32_t y = labels[sample];
+    ys[tid] = y < 0 ? 0 : (y >= C ? C - 1 : y);
+  }
   __syncthreads();
   // logits = bf16(relu(Z1)) bf16(W2) on the matrix cores: wave w takes the
   // 32-unit K steps w, w + 16, .. for both 16-row tiles; the waves' partial
@@ -408,7 +432,7 @@ __global__ void __launch_bounds__(kHeadThreads)
         db1 += v[t];
       }
       const uint2 packed = {pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
-      *reinterpret_cast<uint2*>(dZ1t + ((int64_t)slot * H + hl) * kBatch + r0) = packed;
+      *reinterpret_cast<uint2*>(dZ1t + ((int64_t)blockIdx.x * H + hl) * kBatch + r0) = packed;
     }
     // db1: the four row groups of a unit sit in lanes l, l+16, l+32, l+48
     db1 += __shfl_xor(db1, 16);
@@ -434,10 +458,10 @@ __global__ void __launch_bounds__(kHeadThreads)
   }
 }
 
-// dW1[f][h] = sum_r bf16(A[s_r][f]) bf16(dZ1[r][h]) for one mini-batch
+// dW1[f][h] = sum_r bf16(A[s_r][f]) bf16(dZ1[r][h]) for one list entry
 // (blockIdx.x) and 128 features f0 .. f0+127 (blockIdx.y), every unit h.
 // Computed transposed, D[h][f] = dZ1^T A: the A operand (8 rows r of one
-// unit) is a 16-byte read of the [slot][unit][row] dZ1 copy, the B operand (8
+// unit) is a 16-byte read of the [entry][unit][row] dZ1 copy, the B operand (8
 // rows of one feature) comes from the sample rows staged transposed in LDS,
 // and each lane's four results are consecutive units of one G row: one
 // 16-byte store.  Wave w takes the hidden/64 consecutive unit tiles from
@@ -453,7 +477,7 @@ __global__ void __launch_bounds__(256)
   const int f0 = blockIdx.y * kFeatBlock;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int H = d.hidden;
-  const int64_t row0 = (int64_t)slot * kBatch;
+  const int64_t row0 = (int64_t)blockIdx.x * kBatch;
   // this wave's dZ1 fragments (hidden/64 <= 8 consecutive unit tiles),
   // loaded before the sample rows so both latencies overlap
   const __bf16* dz = dZ1t + row0 * H + 8 * (lane >> 4);  // [unit][row] of this mini-batch
@@ -529,16 +553,15 @@ nbsgd_status check_shape(const nbsgd_mlp_shape* s, Dims* d) {
 
 size_t up256(size_t b) { return (b + 255) & ~(size_t)255; }
 
-// sample list, labels, dZ1 [rows/32][hidden][32] bf16 and kSkMaxSlices partial
-// Z1 planes [rows][hidden] fp32, each 256-byte aligned
+// sample list, dZ1 [rows/32][hidden][32] bf16 and kSkMaxSlices partial Z1
+// planes [rows][hidden] fp32, each 256-byte aligned
 size_t workspace_for(const Dims& d, int64_t rows) {
-  return 2 * up256((size_t)rows * 4) + up256((size_t)rows * d.hidden * 2) +
+  return up256((size_t)rows * 4) + up256((size_t)rows * d.hidden * 2) +
          (size_t)kSkMaxSlices * up256((size_t)rows * d.hidden * 4);
 }
 
 struct Workspace {
   int32_t* idx;
-  int32_t* ylab;
   __bf16* dz1t;
   float* part;        // partial Z1 of each d_in slice
   int64_t part_stride;
@@ -549,8 +572,6 @@ Workspace carve(void* ws, const Dims& d, int64_t rows) {
   Workspace w;
   w.idx = reinterpret_cast<int32_t*>(p);
   p += up256((size_t)rows * 4);
-  w.ylab = reinterpret_cast<int32_t*>(p);
-  p += up256((size_t)rows * 4);
   w.dz1t = reinterpret_cast<__bf16*>(p);
   p += up256((size_t)rows * d.hidden * 2);
   w.part = reinterpret_cast<float*>(p);
@@ -558,10 +579,8 @@ Workspace carve(void* ws, const Dims& d, int64_t rows) {
   return w;
 }
 
-// Copies the sample indices of the mini-batches `slots` (host idx[slot*32 ..])
-// to the workspace through kernel arguments, after checking every one.
-nbsgd_status upload_idx(const int32_t* host, const int32_t* slots, int n_slots, int64_t n_samples,
-                        const int32_t* labels, const Dims& d, const Workspace& w, hipStream_t s) {
+// Checks every sample index of the mini-batches `slots` (host idx[slot*32 ..]).
+nbsgd_status check_idx(const int32_t* host, const int32_t* slots, int n_slots, int64_t n_samples) {
   for (int k = 0; k < n_slots; ++k)
     for (int r = 0; r < kBatch; ++r) {
       const int64_t pos = (int64_t)slots[k] * kBatch + r;
@@ -569,26 +588,31 @@ nbsgd_status upload_idx(const int32_t* host, const int32_t* slots, int n_slots, 
         return fail(NBSGD_E_ARG, "sample index %d at position %lld is outside [0, %lld)", host[pos],
                     (long long)pos, (long long)n_samples);
     }
-  const int wide = n_samples > 65536 ? 1 : 0;
+  return NBSGD_OK;
+}
+
+// Copies the sample indices of list entries 0 .. count-1 (host idx[slot*32 ..]
+// of entry e's slot mb[e].second) to the workspace rows e*32 .. through the
+// kernel arguments of k_put_idx.
+void put_idx(const int32_t* host, const std::pair<int, int>* mb, int count, bool wide,
+             const Workspace& w, hipStream_t s) {
   const int per = wide ? kUpSlots / 2 : kUpSlots;
-  for (int k0 = 0; k0 < n_slots; k0 += per) {
+  for (int k0 = 0; k0 < count; k0 += per) {
     IdxChunk c;
     memset(&c, 0, sizeof(c));
-    c.n_slots = std::min(per, n_slots - k0);
-    c.wide = wide;
+    c.first = k0;
+    c.n_slots = std::min(per, count - k0);
+    c.wide = wide ? 1 : 0;
     for (int k = 0; k < c.n_slots; ++k) {
-      c.slot[k >> 1] |= (uint32_t)slots[k0 + k] << (16 * (k & 1));
-      const int32_t* src = host + (int64_t)slots[k0 + k] * kBatch;
+      const int32_t* src = host + (int64_t)mb[k0 + k].second * kBatch;
       for (int r = 0; r < kBatch; ++r) {
         const int t = k * kBatch + r;
         if (wide) c.v[t] = (uint32_t)src[r];
         else c.v[t >> 1] |= (uint32_t)src[r] << (16 * (t & 1));
       }
     }
-    hipLaunchKernelGGL(k_put_idx, dim3((c.n_slots * kBatch + 255) / 256), dim3(256), 0, s, w.idx,
-                       w.ylab, labels, d.classes, c);
+    hipLaunchKernelGGL(k_put_idx, dim3((c.n_slots * kBatch + 255) / 256), dim3(256), 0, s, w.idx, c);
   }
-  return NBSGD_OK;
 }
 
 nbsgd_status launch_err(const char* what) {
@@ -599,11 +623,15 @@ nbsgd_status launch_err(const char* what) {
 
 uint32_t item(int learner, int slot) { return ((uint32_t)learner << 24) | ((uint32_t)slot << 12); }
 
-// Launches the three kernels over mini-batches `mb` (learner, slot), sorted
-// by learner, of one group (at most kMaxList).
+// Launches the kernels over mini-batches `mb` (learner, slot), sorted by
+// learner, of one group (at most kMaxList): the sample indices host_idx[slot
+// * 32 ..] (checked) go to the workspace in the forward kernel's arguments
+// when the group has at most kInline mini-batches and they fit 16 bits
+// (`wide` false), otherwise through k_put_idx first.
 template <bool BACKWARD>
-void launch_group(const std::pair<int, int>* mb, int count, const float* X, const float* data,
-                  const Workspace& w, float* G, float* losses, const Dims& d, hipStream_t st) {
+void launch_group(const std::pair<int, int>* mb, int count, const int32_t* host_idx, bool wide,
+                  const float* X, const float* data, const int32_t* labels, const Workspace& w,
+                  float* G, float* losses, const Dims& d, hipStream_t st) {
   List items;
   items.count = count;
   for (int k = 0; k < count; ++k) items.w[k] = item(mb[k].first, mb[k].second);
@@ -624,18 +652,35 @@ void launch_group(const std::pair<int, int>* mb, int count, const float* X, cons
       if (K.n > 0) sk_total += K.S * K.ub * ((k - K.first[K.n - 1] + 3) / 4);
       K.off[K.n] = sk_total;
       K.first[K.n] = k;
+      K.learner[K.n >> 2] |= (uint32_t)item_learner(items.w[k]) << (8 * (K.n & 3));
       ++K.n;
     }
   }
   sk_total += K.S * K.ub * ((items.count - K.first[K.n - 1] + 3) / 4);
   K.off[K.n] = sk_total;
   K.first[K.n] = items.count;
-  for (int x = 0; x <= 8; ++x) K.xcd_start[x] = (int32_t)((int64_t)x * sk_total / 8);
-  const int sk_per_xcd = (sk_total + 7) / 8;
-  hipLaunchKernelGGL(k_mlp_fwd_sk, dim3(8 * sk_per_xcd), dim3(512), 0, st, X, data, w.idx, w.part,
-                     w.part_stride, d, K, items);
-  hipLaunchKernelGGL(k_mlp_head<BACKWARD>, dim3(items.count), dim3(kHeadThreads), 0, st, X, w.ylab,
-                     w.part, w.part_stride, K.S, w.dz1t, G, losses, d, items);
+  // each XCD's range of work items holds at most ceil(total / 8)
+  const dim3 fgrid(8 * ((sk_total + 7) / 8));
+  if (!wide && count <= kInline) {
+    InlineIdx I;
+    memset(&I, 0, sizeof I);
+    for (int e = 0; e < count; ++e) {
+      const int32_t* src = host_idx + (int64_t)mb[e].second * kBatch;
+      for (int r = 0; r < kBatch; ++r) {
+        const int t = e * kBatch + r;
+        I.v[t >> 1] |= (uint32_t)src[r] << (16 * (t & 1));
+      }
+    }
+    hipLaunchKernelGGL(k_mlp_fwd_sk<true>, fgrid, dim3(512), 0, st, X, data, w.idx, w.part,
+                       w.part_stride, d, K, I);
+  } else {
+    put_idx(host_idx, mb, count, wide, w, st);
+    const Idx16<1> none = {{0u}};
+    hipLaunchKernelGGL(k_mlp_fwd_sk<false>, fgrid, dim3(512), 0, st, X, data, w.idx, w.part,
+                       w.part_stride, d, K, none);
+  }
+  hipLaunchKernelGGL(k_mlp_head<BACKWARD>, dim3(items.count), dim3(kHeadThreads), 0, st, X, w.idx,
+                     labels, w.part, w.part_stride, K.S, w.dz1t, G, losses, d, items);
   if (BACKWARD)
     hipLaunchKernelGGL(k_mlp_wgrad, dim3(items.count, d.d_in / kFeatBlock), dim3(256), 0, st, data,
                        w.idx, w.dz1t, G, d, items);
@@ -690,18 +735,18 @@ nbsgd_status mlp_grad_impl(const float* X, int64_t ld, int32_t n, int32_t m,
   std::vector<int32_t> finished;
   for (int32_t k = 0; k < n * m; ++k)
     if (mask[k]) finished.push_back(k);
-  if (nbsgd_status r = upload_idx(idx, finished.data(), (int)finished.size(), n_samples, labels, d, w, st))
-    return r;
+  if (nbsgd_status r = check_idx(idx, finished.data(), (int)finished.size(), n_samples)) return r;
+  const bool wide = n_samples > 65536;
   std::pair<int, int> mb[kMaxList];
   int count = 0;
   for (int32_t k : finished) {
     mb[count++] = {k / m, k};
     if (count == kMaxList) {
-      launch_group<true>(mb, count, X, data, w, G, losses, d, st);
+      launch_group<true>(mb, count, idx, wide, X, data, labels, w, G, losses, d, st);
       count = 0;
     }
   }
-  if (count) launch_group<true>(mb, count, X, data, w, G, losses, d, st);
+  if (count) launch_group<true>(mb, count, idx, wide, X, data, labels, w, G, losses, d, st);
   return launch_err("nbsgd_mlp_grad");
 }
 
@@ -755,7 +800,8 @@ extern "C" nbsgd_status nbsgd_mlp_loss(const float* params, const nbsgd_mlp_shap
     mb[k] = {0, k};
     slots[k] = k;
   }
-  if (nbsgd_status r = upload_idx(idx, slots, count / kBatch, n_samples, labels, d, w, st)) return r;
-  launch_group<false>(mb, count / kBatch, params, data, w, nullptr, losses, d, st);
+  if (nbsgd_status r = check_idx(idx, slots, count / kBatch, n_samples)) return r;
+  launch_group<false>(mb, count / kBatch, idx, n_samples > 65536, params, data, labels, w, nullptr,
+                      losses, d, st);
   return launch_err("nbsgd_mlp_loss");
 }

@@ -325,6 +325,51 @@ def test_grad_two_launch_groups_and_wide_indices():
     assert (r.G[3, 10:] == 7.0).all() and (r.G[15, 1:] == 7.0).all()
 
 
+@pytest.mark.parametrize("finished", [56, 57])
+def test_grad_indices_in_arguments_match_indices_through_workspace(finished):
+    """Up to 56 finished mini-batches travel with their sample indices in the
+    forward kernel's arguments; more go through the workspace first.  Every
+    mini-batch's gradient and loss depend only on its own samples and
+    replica, so a call with 56 (or 57) finished and one with all 64 agree bit
+    for bit on the common entries; the 64-entry call is also checked against
+    the oracle on sampled entries."""
+    n, m, n_samples, dims = 8, 8, 300, (256, 128, 10)
+    s = Shape(*dims, 32)
+    A = mlp_data.inputs(11, n_samples, dims[0])
+    y = mlp_data.teacher_labels(11, A, dims[1], dims[2])
+    x0 = mlp_data.student_init(11, *dims)
+    rng = np.random.default_rng(finished)
+    X = (x0[None, :] + 0.05 * rng.standard_normal((n, s.n_params))).astype(np.float32)
+    idx = rng.integers(0, n_samples, size=(n, m, 32)).astype(np.int32)
+    part = np.zeros(n * m, np.uint8)
+    part[rng.permutation(n * m)[:finished]] = 1
+    part = part.reshape(n, m)
+    full = np.ones((n, m), np.uint8)
+    _say(f"mlp grad indices in arguments / workspace, finished={finished} and 64")
+    P = _lib.mlp_param_count(*dims)
+    Xd = torch.from_numpy(pad_cols(X, P)).to(DEV)
+    data = torch.from_numpy(A).to(DEV)
+    labels = torch.from_numpy(y.astype(np.int32)).to(DEV)
+    ws = torch.empty((_lib.mlp_workspace_bytes(*dims, n * m * 32) + 15) // 16 * 4,
+                     dtype=torch.float32, device=DEV)
+    out = {}
+    for name, mask in (("part", part), ("full", full)):
+        G = torch.full((n, m, P), 7.0, dtype=torch.float32, device=DEV)
+        losses = torch.full((n * m,), -1.0, dtype=torch.float32, device=DEV)
+        _lib.mlp_grad(Xd, m, dims, data, labels, idx, mask, G, losses, ws)
+        torch.cuda.synchronize()
+        out[name] = (G.cpu().numpy(), losses.cpu().numpy().reshape(n, m))
+    Gp, Lp = out["part"]
+    Gf, Lf = out["full"]
+    done = part.astype(bool)
+    assert np.array_equal(Gp[done], Gf[done]) and np.array_equal(Lp[done], Lf[done])
+    assert (Gp[~done] == 7.0).all() and (Lp[~done] == -1.0).all()
+    for i, j in ((0, 0), (3, 5), (7, 7)):
+        g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
+        assert rel_err_blocks(Gf[i, j], g, mlp_blocks(*dims)) <= TOL_BF16, (i, j)
+        assert abs(Lf[i, j] - loss) <= TOL_BF16 * abs(loss)
+
+
 def test_loss_odd_batch_count(tiny):
     """Three batches: the forward pairs two of them in one tile and leaves
     the third alone."""
