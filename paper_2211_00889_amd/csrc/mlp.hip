@@ -307,37 +307,53 @@ __global__ void __launch_bounds__(kHeadThreads)
   const int64_t row0 = (int64_t)blockIdx.x * kBatch;
   const int32_t sample = tid < kBatch ? idx[row0 + tid] : 0;  // loaded ahead of its use
 
-  // Z1: thread takes row tid / TPR and units 4 (tid % TPR) + SPAN j
+  // Z1: thread takes row tid / TPR and units uq + SPAN j, uq = 4 (tid % TPR).
+  // Every load of this phase (the slices, b1, W2 and the label) is issued
+  // before any of them is used, so the phase costs one memory round trip.
   constexpr int TPR = kHeadThreads / 32, SPAN = 4 * TPR;
+  constexpr int kW2Loads = kMaxHidden * kMaxClasses / kHeadThreads;
+  static_assert(4 * SPAN >= kMaxHidden && kW2Loads * kHeadThreads == kMaxHidden * kMaxClasses,
+                "one pass of the phase covers every unit and every W2 entry");
+  float b2v;  // b2 of class tid % 16, for the softmax thread (row tid / 16, class tid % 16)
   {
     const int r = tid / TPR, uq = 4 * (tid % TPR);
     const float* src = Zpart + (row0 + r) * H + uq;
-    for (int j0 = 0; j0 * SPAN < H; j0 += 4) {
-      f32x4 p[kSkMaxSlices][4];
+    f32x4 p[kSkMaxSlices][4], b[4];
 #pragma unroll
-      for (int q = 0; q < kSkMaxSlices; ++q)
+    for (int q = 0; q < kSkMaxSlices; ++q)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          p[q][j] = (q < S && uq + SPAN * (j0 + j) < H)
-                        ? *reinterpret_cast<const f32x4*>(src + (int64_t)q * part_stride + SPAN * (j0 + j))
-                        : f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < 4; ++j)
+        p[q][j] = (q < S && uq + SPAN * j < H)
+                      ? *reinterpret_cast<const f32x4*>(src + (int64_t)q * part_stride + SPAN * j)
+                      : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (uq + SPAN * (j0 + j) >= H) break;
-        const int u = uq + SPAN * (j0 + j);
-        f32x4 z = p[0][j];
+    for (int j = 0; j < 4; ++j)
+      b[j] = uq + SPAN * j < H ? *reinterpret_cast<const f32x4*>(prm + d.off_b1 + uq + SPAN * j)
+                               : f32x4{0.f, 0.f, 0.f, 0.f};
+    float w2[kW2Loads];
 #pragma unroll
-        for (int q = 1; q < kSkMaxSlices; ++q)
-          if (q < S) z += p[q][j];
-        z += *reinterpret_cast<const f32x4*>(prm + d.off_b1 + u);
-        *reinterpret_cast<f32x4*>(Z1s + r * kLdz + u) = z;
-      }
+    for (int k = 0; k < kW2Loads; ++k) {
+      const int e = tid + k * kHeadThreads;
+      w2[k] = e < H * C ? prm[d.off_w2 + e] : 0.0f;
     }
-  }
-  for (int k = tid; k < H * C; k += kHeadThreads) W2s[k] = bf16r(prm[d.off_w2 + k]);
-  if (tid < kBatch) {
-    const int32_t y = labels[sample];
-    ys[tid] = y < 0 ? 0 : (y >= C ? C - 1 : y);
+    const int32_t y = tid < kBatch ? labels[sample] : 0;
+    b2v = tid < kBatch * 16 && (tid & 15) < C ? prm[d.off_b2 + (tid & 15)] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (uq + SPAN * j >= H) break;
+      f32x4 z = p[0][j];
+#pragma unroll
+      for (int q = 1; q < kSkMaxSlices; ++q)
+        if (q < S) z += p[q][j];
+      z += b[j];
+      *reinterpret_cast<f32x4*>(Z1s + r * kLdz + uq + SPAN * j) = z;
+    }
+#pragma unroll
+    for (int k = 0; k < kW2Loads; ++k) {
+      const int e = tid + k * kHeadThreads;
+      if (e < H * C) W2s[e] = bf16r(w2[k]);
+    }
+    if (tid < kBatch) ys[tid] = y < 0 ? 0 : (y >= C ? C - 1 : y);
   }
   __syncthreads();
   // logits = bf16(relu(Z1)) bf16(W2) on the matrix cores: wave w takes the
@@ -368,28 +384,30 @@ __global__ void __launch_bounds__(kHeadThreads)
         Lp[(wave * kBatch + 16 * rt + 4 * (lane >> 4) + t) * 16 + cl] = acc[rt][t];
   }
   __syncthreads();
-  if (tid < kBatch * C) {
-    const int r = tid / C, c = tid % C;
+  // softmax cross-entropy, thread (row tid / 16, class tid % 16): the logit
+  // (the waves' partial sums in wave order, + b2), then the row's max and sum
+  // of exponentials over the 16 lanes of the row by xor butterflies (every
+  // lane of a row ends with the same sums)
+  if (tid < kBatch * 16) {
+    const int r = tid >> 4, c = tid & 15;
+    const bool live = c < C;
     float z = 0.0f;
     for (int w = 0; w < kHeadThreads / 64; ++w) z += Lp[(w * kBatch + r) * 16 + c];
-    Zs[r * kMaxClasses + c] = z + prm[d.off_b2 + c];
-  }
-  __syncthreads();
-  if (tid < kBatch) {
-    const int r = tid;
-    const float* z = Zs + r * kMaxClasses;
-    float zmax = z[0];
-    for (int c = 1; c < C; ++c) zmax = fmaxf(zmax, z[c]);
-    float sum = 0.0f;
-    for (int c = 0; c < C; ++c) sum += expf(z[c] - zmax);
+    z += b2v;
+    float zmax = live ? z : -INFINITY;
+#pragma unroll
+    for (int o = 8; o; o >>= 1) zmax = fmaxf(zmax, __shfl_xor(zmax, o, 16));
+    float sum = live ? expf(z - zmax) : 0.0f;
+#pragma unroll
+    for (int o = 8; o; o >>= 1) sum += __shfl_xor(sum, o, 16);
     const float lse = zmax + logf(sum);
-    row_loss[r] = lse - z[ys[r]];
-    if (BACKWARD)
-      for (int c = 0; c < kMaxClasses; ++c) {
-        const float g = c < C ? (expf(z[c] - lse) - (c == ys[r] ? 1.0f : 0.0f)) * (1.0f / kBatch) : 0.0f;
-        Zs[r * kMaxClasses + c] = g;
-        Zb[r * kMaxClasses + c] = bf16r(g);
-      }
+    const int yr = ys[r];
+    if (c == yr) row_loss[r] = lse - z;
+    if (BACKWARD) {
+      const float g = live ? (expf(z - lse) - (c == yr ? 1.0f : 0.0f)) * (1.0f / kBatch) : 0.0f;
+      Zs[r * kMaxClasses + c] = g;
+      Zb[r * kMaxClasses + c] = bf16r(g);
+    }
   }
   __syncthreads();
   float* g = G + (int64_t)slot * d.ld;
