@@ -325,15 +325,16 @@ def test_grad_two_launch_groups_and_wide_indices():
     assert (r.G[3, 10:] == 7.0).all() and (r.G[15, 1:] == 7.0).all()
 
 
+@pytest.mark.parametrize("dims", [(256, 128, 10), (3072, 512, 10)])
 @pytest.mark.parametrize("finished", [56, 57])
-def test_grad_indices_in_arguments_match_indices_through_workspace(finished):
+def test_grad_indices_in_arguments_match_indices_through_workspace(finished, dims):
     """Up to 56 finished mini-batches travel with their sample indices in the
     forward kernel's arguments; more go through the workspace first.  Every
     mini-batch's gradient and loss depend only on its own samples and
     replica, so a call with 56 (or 57) finished and one with all 64 agree bit
     for bit on the common entries; the 64-entry call is also checked against
     the oracle on sampled entries."""
-    n, m, n_samples, dims = 8, 8, 300, (256, 128, 10)
+    n, m, n_samples = 8, 8, 300
     s = Shape(*dims, 32)
     A = mlp_data.inputs(11, n_samples, dims[0])
     y = mlp_data.teacher_labels(11, A, dims[1], dims[2])
@@ -345,7 +346,7 @@ def test_grad_indices_in_arguments_match_indices_through_workspace(finished):
     part[rng.permutation(n * m)[:finished]] = 1
     part = part.reshape(n, m)
     full = np.ones((n, m), np.uint8)
-    _say(f"mlp grad indices in arguments / workspace, finished={finished} and 64")
+    _say(f"mlp grad indices in arguments / workspace, dims={dims} finished={finished} and 64")
     P = _lib.mlp_param_count(*dims)
     Xd = torch.from_numpy(pad_cols(X, P)).to(DEV)
     data = torch.from_numpy(A).to(DEV)
