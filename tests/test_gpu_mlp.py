@@ -371,6 +371,29 @@ def test_grad_indices_in_arguments_match_indices_through_workspace(finished, dim
         assert abs(Lf[i, j] - loss) <= TOL_BF16 * abs(loss)
 
 
+def test_grad_largest_16_bit_sample_index():
+    """65,536 samples: every index fits 16 bits, so the indices ride in the
+    forward kernel's arguments, the largest one (65,535) included."""
+    wl = dataclasses.replace(workloads.MLP_TINY, n_samples=65_536)
+    s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
+    A, y, x0 = _data(wl)
+    rng = np.random.default_rng(9)
+    X = (x0[None, :] + 0.05 * rng.standard_normal((wl.n, s.n_params))).astype(np.float32)
+    mask = np.ones((wl.n, wl.m), np.uint8)
+    idx = rng.integers(0, wl.n_samples, size=(wl.n, wl.m, wl.batch)).astype(np.int32)
+    idx[2, 3, :] = wl.n_samples - 1 - np.arange(wl.batch)
+    _say(f"mlp grad n_samples={wl.n_samples} largest index {wl.n_samples - 1}")
+    r = runner.MlpRunner(wl, DEV, A, y, x0)
+    Xd = torch.from_numpy(pad_cols(X, r.P)).to(DEV)
+    _lib.mlp_grad(Xd, wl.m, r.dims, r.data, r.labels, idx, mask, r.G, r.losses, r.workspace)
+    torch.cuda.synchronize()
+    L = r.losses.cpu().numpy().reshape(wl.n, wl.m)
+    for i, j in ((2, 3), (0, 0), (wl.n - 1, wl.m - 1)):
+        g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
+        assert rel_err_blocks(r.G[i, j].cpu().numpy(), g, mlp_blocks(*r.dims)) <= TOL_BF16, (i, j)
+        assert abs(L[i, j] - loss) <= TOL_BF16 * abs(loss)
+
+
 def test_loss_odd_batch_count(tiny):
     """Three batches: the forward pairs two of them in one tile and leaves
     the third alone."""
