@@ -92,29 +92,26 @@ def measured_traffic(wl):
 
 def cpu_baseline(wl, budget_s: float = 15.0, cols: int = 1 << 19):
     """The oracle on columns [0, cols) of the workload, one thread, about
-    ``budget_s`` seconds; returns learner-param updates per second."""
+    ``budget_s`` seconds; returns learner-param updates per second (the step
+    is column-separable, so the cost per column is constant and the rate
+    scales to the full P)."""
     from threadpoolctl import threadpool_limits
 
-    import oracle
-    from tests._util import ORACLE_ORDER, OracleMixer, oracle_delay, window_inputs
+    import oracle.workload
 
     cols = min(cols, wl.P)
-    X0, G = window_inputs(wl, np.arange(cols))
-    X = X0.astype(np.float64)
-    V = np.zeros_like(X)
-    mixer, d = OracleMixer(wl), oracle_delay(wl)
-    lr, mu = float(np.float32(wl.lr)), float(np.float32(wl.momentum))
-    steps = 0
+    X0, G = oracle.workload.window_inputs(wl, np.arange(cols))
+    done = []
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
-        while True:
-            s = oracle.schedule.sample_schedule(wl.seed, steps, wl.n, wl.m, d)
-            X, V = oracle.step.step(X, V, G, s["mask"], mixer.w(steps), lr, mu,
-                                    ORACLE_ORDER[wl.order])
-            steps += 1
-            el = time.perf_counter() - t0
-            if el >= budget_s:
-                break
+
+        def stop(k):
+            done.append(k)
+            return time.perf_counter() - t0 >= budget_s
+
+        oracle.workload.run(wl, X0, G, 1 << 30, stop=stop)
+        el = time.perf_counter() - t0
+    steps = len(done)
     return {"value": wl.n * cols * steps / el, "unit": UNIT, "cores": 1, "kind": "oracle",
             "sample": f"{wl.name}: columns [0, {cols}) of P={wl.P}, {steps} steps in {el:.1f} s "
                       f"(fp64 NumPy, 1 thread; the step is column-separable so per-column cost "
@@ -125,42 +122,18 @@ def cpu_baseline_mlp(wl, A, y, x0, budget_s: float = 15.0):
     """The oracle's MLP iterations (schedule, the bf16-input gradient of every
     finished mini-batch in fp64, the step), one thread, whole iterations until
     ``budget_s`` has passed; returns finished training samples per second.
-    The oracle's evaluations of the average replica are not timed."""
+    The oracle's evaluations of the average replica are left out."""
     from threadpoolctl import threadpool_limits
 
-    import oracle
-    from oracle.mlp import BF16, Shape
+    import oracle.mlp
 
-    s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
-    n, m, P = wl.n, wl.m, s.n_params
-    kinds = {"const": oracle.schedule.DELAY_CONST, "exp": oracle.schedule.DELAY_EXP,
-             "lomax": oracle.schedule.DELAY_LOMAX}
-    d = oracle.schedule.Delay(kinds[wl.delay.kind], wl.delay.base, wl.delay.param,
-                              wl.delay.slow_learner, wl.delay.slow_factor, wl.delay.slow_prob)
-    W = oracle.mixing.w_ring(n).astype(np.float32).astype(np.float64)
-    order = (oracle.step.MIX_THEN_STEP if wl.order == "mix_then_step"
-             else oracle.step.STEP_THEN_MIX)
-    lr, mu = float(np.float32(wl.lr)), float(np.float32(wl.momentum))
-    shuf = oracle.mlp.Shuffler(wl.seed, wl.n_samples // n, m, wl.batch)
-    X = np.tile(np.asarray(x0, dtype=np.float64), (n, 1))
-    V = np.zeros_like(X)
-    G = np.zeros((n, m, P))
-    finished, k = 0, 0
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
-        while True:
-            sch = oracle.schedule.sample_schedule(wl.seed, k, n, m, d)
-            for i in range(n):
-                idx = shuf.indices(k, i)
-                for j in range(m):
-                    if sch["mask"][i, j]:
-                        G[i, j] = oracle.mlp.grad(X[i], A[idx[j]], y[idx[j]], s, BF16)[0]
-            X, V = oracle.step.step(X, V, G, sch["mask"], W, lr, mu, order)
-            finished += int(sch["mask"].sum())
-            k += 1
-            el = time.perf_counter() - t0
-            if el >= budget_s:
-                break
+        out = oracle.mlp.train(wl, A, y, x0, 1 << 30, evaluate=False,
+                               stop=lambda k: time.perf_counter() - t0 >= budget_s)
+        el = time.perf_counter() - t0
+    finished = int(sum(int(c.sum()) for c in out["counts"]))
+    k = out["iterations"]
     return {"value": finished * wl.batch / el, "unit": "samples/s", "cores": 1, "kind": "oracle",
             "sample": f"{wl.name}: iterations 0..{k - 1} ({finished} finished mini-batches) in "
                       f"{el:.1f} s (fp64 NumPy with bf16-rounded GEMM inputs, 1 thread; "
@@ -362,12 +335,80 @@ def bench_unfused(args):
         "kernels": per}), flush=True)
 
 
+def time_step_workload(wl, args, dev):
+    """Times K back-to-back fused steps of a step workload after W warm-up
+    steps, on resident buffers; returns the figures of one bench record."""
+    import torch
+
+    from paper_2211_00889_amd import runner
+
+    r = runner.StepRunner(wl, dev)
+    stream = torch.cuda.current_stream(dev)
+    for k in range(args.warmup):
+        mask, counts, _, W = r.plan(k)
+        r.launch(mask, W)
+    torch.cuda.synchronize()
+
+    # Two events bracket the K launches on their stream: the launches run back
+    # to back, so (end - start) / K is the kernel's mean launch duration.  An
+    # event pair around every launch would put two event packets between
+    # consecutive kernels (about 10 us per step on a 0.55 ms kernel).
+    K = args.steps
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    sum_counts, plan_s = [], []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for i in range(K):
+        t_plan = time.perf_counter()
+        mask, counts, _, W = r.plan(args.warmup + i)
+        plan_s.append(time.perf_counter() - t_plan)
+        r.launch(mask, W)
+        sum_counts.append(int(counts.sum()))
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ld = r.ld
+    del r
+    torch.cuda.empty_cache()
+
+    kern_ms_mean = start.elapsed_time(end) / K
+    alg_bytes = np.array([wl.alg_bytes(c) for c in sum_counts], dtype=np.float64)
+    achieved = alg_bytes.sum() / (kern_ms_mean * K * 1e-3) / 1e9
+    rec = {
+        "value": wl.n * wl.P * K / wall,
+        "ms_per_step": wall * 1e3 / K,
+        "config": {"workload": wl.name, "n_learners": wl.n, "minibatches": wl.m, "P": wl.P,
+                   "row_stride": ld, "mixing": wl.mixing, "order": wl.order,
+                   "delay": wl.delay.kind, "lr": wl.lr, "momentum": wl.momentum,
+                   "mean_finished_per_step": float(np.mean(sum_counts))},
+        "host_plan_us": float(np.mean(plan_s) * 1e6),
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "kernel": "k_step", "kernel_ms_mean": float(kern_ms_mean),
+                     "kernel_ms_of": "HIP events around the K back-to-back launches, divided by K",
+                     "alg_bytes_per_launch_mean": float(alg_bytes.mean())},
+    }
+    tr = measured_traffic(wl)
+    if tr is not None:
+        rec["roofline"]["traffic"] = tr["traffic_bytes_per_launch"]
+        rec["roofline"]["traffic_over_alg"] = tr["traffic_over_alg"]
+        rec["roofline"]["traffic_dispatches"] = f"{tr['dispatches']} launches, steps {tr['steps']}"
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="resnet18")
+    ap.add_argument("--workload", default="vgg16",
+                    help="the headline step workload (default: the VGG-16-sized one, the largest "
+                         "that fits one GPU), or mlp for the end-to-end MLP workload")
+    ap.add_argument("--also", default=None,
+                    help="comma-separated step workloads timed after the headline one in the same "
+                         "run and reported under other_configs (default with --workload vgg16: "
+                         "resnet18,resnet50; 'none' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--unfused", action="store_true",
                     help="time the three unfused stages instead of the fused step")
@@ -396,21 +437,20 @@ def main():
 
     import torch
 
-    from paper_2211_00889_amd import runner
     from synth import workloads
 
     wl = workloads.get(args.workload)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    r = runner.StepRunner(wl, dev)
-    stream = torch.cuda.current_stream(dev)
-
-    for k in range(args.warmup):
-        mask, counts, _, W = r.plan(k)
-        r.launch(mask, W)
-    torch.cuda.synchronize()
 
     if args.graph:
+        from paper_2211_00889_amd import runner
+
+        r = runner.StepRunner(wl, dev)
+        for k in range(args.warmup):
+            mask, counts, _, W = r.plan(k)
+            r.launch(mask, W)
+        torch.cuda.synchronize()
         out = bench_graph(args, wl, r, dev)
         del r
         torch.cuda.empty_cache()
@@ -419,64 +459,27 @@ def main():
         print(json.dumps(out), flush=True)
         return
 
-    # Two events bracket the K launches on their stream: the launches run back
-    # to back, so (end - start) / K is the kernel's mean launch duration.  An
-    # event pair around every launch would put two event packets between
-    # consecutive kernels (about 10 us per step on a 0.55 ms kernel).
-    K = args.steps
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    sum_counts = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    plan_s = []
-    start.record(stream)
-    for i in range(K):
-        t_plan = time.perf_counter()
-        mask, counts, _, W = r.plan(args.warmup + i)
-        plan_s.append(time.perf_counter() - t_plan)
-        r.launch(mask, W)
-        sum_counts.append(int(counts.sum()))
-    end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-
-    kern_ms_mean = start.elapsed_time(end) / K
-    alg_bytes = np.array([wl.alg_bytes(c) for c in sum_counts], dtype=np.float64)
-    achieved = alg_bytes.sum() / (kern_ms_mean * K * 1e-3) / 1e9
-    value = wl.n * wl.P * K / wall
+    head = time_step_workload(wl, args, dev)
+    print(f"[bench] {wl.name}: {head['roofline']['kernel_ms_mean']:.4f} ms per step, "
+          f"{head['roofline']['frac']:.3f} of peak", file=sys.stderr, flush=True)
     out = {
         "metric": METRIC,
-        "value": value,
+        "value": head["value"],
         "unit": UNIT,
         "n_gpus": 1,
-        "steps": K,
+        "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": wall * 1e3 / K,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded SplitMix64 Irwin-Hall normals: X ~ N(0, 1), G ~ N(0, 1e-3))",
-        "config": {"workload": wl.name, "n_learners": wl.n, "minibatches": wl.m, "P": wl.P,
-                   "row_stride": r.ld,
-                   "mixing": wl.mixing, "order": wl.order, "delay": wl.delay.kind,
-                   "lr": wl.lr, "momentum": wl.momentum,
-                   "mean_finished_per_step": float(np.mean(sum_counts))},
-        "host_plan_us": float(np.mean(plan_s) * 1e6),
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBS, "traffic": None,
-                     "kernel": "k_step", "kernel_ms_mean": float(kern_ms_mean),
-                     "kernel_ms_of": "HIP events around the K back-to-back launches, divided by K",
-                     "alg_bytes_per_launch_mean": float(alg_bytes.mean())},
+        "config": head["config"],
+        "host_plan_us": head["host_plan_us"],
+        "roofline": head["roofline"],
     }
-    rec = measured_traffic(wl)
-    if rec is not None:
-        out["roofline"]["traffic"] = rec["traffic_bytes_per_launch"]
-        out["roofline"]["traffic_over_alg"] = rec["traffic_over_alg"]
-        out["roofline"]["traffic_dispatches"] = f"{rec['dispatches']} launches, steps {rec['steps']}"
-    del r
-    torch.cuda.empty_cache()
-    out["copy_context"] = copy_context(int(alg_bytes.mean()) // 2, dev)
+    out["copy_context"] = copy_context(int(head["roofline"]["alg_bytes_per_launch_mean"]) // 2, dev)
     if args.calibration_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
@@ -484,6 +487,27 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+        torch.cuda.empty_cache()
+    also = args.also
+    if also is None:
+        also = "resnet18,resnet50" if wl.name == workloads.VGG16_ALLREDUCE.name else "none"
+    others = []
+    for name in [a for a in also.split(",") if a and a != "none"]:
+        w = workloads.get(name)
+        rec = time_step_workload(w, args, dev)
+        print(f"[bench] {w.name}: {rec['roofline']['kernel_ms_mean']:.4f} ms per step, "
+              f"{rec['roofline']['frac']:.3f} of peak", file=sys.stderr, flush=True)
+        rf = rec["roofline"]
+        others.append({"workload": w.name, "value": rec["value"], "unit": UNIT,
+                       "ms_per_step": rec["ms_per_step"], "kernel": "k_step",
+                       "kernel_ms_mean": rf["kernel_ms_mean"],
+                       "alg_bytes_per_launch_mean": rf["alg_bytes_per_launch_mean"],
+                       "achieved_GBs": rf["achieved"], "frac": rf["frac"],
+                       "traffic_over_alg": rf.get("traffic_over_alg"),
+                       "mean_finished_per_step": rec["config"]["mean_finished_per_step"],
+                       "row_stride": rec["config"]["row_stride"]})
+    if others:
+        out["other_configs"] = others
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -115,9 +115,36 @@ nbsgd_status nbsgd_sample_mask(uint64_t seed, uint64_t step, int32_t n, int32_t 
                                const nbsgd_delay *d, uint8_t *mask, int32_t *counts,
                                double *times, double *timing);
 
+/* -------------------------------------------------- Sec. 4.3 accounting
+ * Throughput accounting of one iteration (Thm 3-5, Cor. 1) from its
+ * per-mini-batch times (the `times` output of nbsgd_sample_mask), in units of
+ * mini-batches: a learner's batch B is its m mini-batches.  Learner i's batch
+ * time is X_i = sum_j times[i*m+j] (summed in mini-batch order); X_{1:P} <=
+ * ... <= X_{P:P} are the X_i sorted, and Y = sum_k 1 / X_{k:P}, summed from
+ * the fastest learner.
+ *   x_first          X_{1:P}: the non-blocking iteration time (the terminal
+ *                    signal, T of nbsgd_sample_mask)
+ *   x_last           X_{P:P}: the blocking iteration time (T_sync)
+ *   y                Y
+ *   throughput       Thm 3: B * Y, non-blocking mini-batches per time unit
+ *   throughput_sync  Thm 4: P * B / X_{P:P}, the blocking baseline's
+ *   data             Cor. 1: B * Y * X_{1:P}, the fractional number of
+ *                    mini-batches one non-blocking iteration trains when
+ *                    every learner runs at a constant speed within it
+ *   ratio            Thm 5: Y * X_{P:P} / P, non-blocking over blocking
+ *                    throughput (>= 1)
+ * times  host double [n*m], finite and >= 0, every learner's sum > 0.
+ * Errors: NBSGD_E_ARG (null pointer, a negative or non-finite time, a zero
+ *         batch time), NBSGD_E_SHAPE, NBSGD_E_UNSUPPORTED.                    */
+typedef struct {
+  double x_first, x_last, y, throughput, throughput_sync, data, ratio;
+} nbsgd_accounting;
+nbsgd_status nbsgd_iteration_accounting(const double *times, int32_t n, int32_t m,
+                                        nbsgd_accounting *out);
+
 /* ------------------------------------------------------------- accumulate
  * Accumulated gradient of the finished mini-batches (Alg. 2 mini-batch loop;
- * Sec. 3.2 "compute gradients"), normalised by the finished count:
+ * Sec. 3.2, gradient bullet), normalised by the finished count:
  *   Gbar[i][:] = (1 / c_i) * sum_{j : mask[i*m+j] != 0} G[i][j][:]
  * G     device fp32 [n][m][P] (only finished rows are read)
  * mask  host uint8 [n*m], any pattern; c_i = number of nonzero entries >= 1
@@ -142,8 +169,8 @@ nbsgd_status nbsgd_mix(const float *X, const float *W, int32_t n, int64_t P, flo
                        void *stream);
 
 /* ----------------------------------------------------------------- update
- * Local step with the finished-fraction learning rate (Sec. 3.2 "adjust
- * learning rate" and "gradient update") and heavy-ball momentum:
+ * Local step with the finished-fraction learning rate (Sec. 3.2, learning-rate
+ * and update bullets) and heavy-ball momentum:
  *   eta_i = lr * counts[i] / m   (fp64, rounded once to fp32)
  *   V[i] = momentum * V[i] + Gbar[i];   X[i] = X[i] - eta_i * V[i]
  * X, V  device fp32 [n][P], updated in place
@@ -279,8 +306,8 @@ nbsgd_status nbsgd_mlp_param_count(const nbsgd_mlp_shape *s, int64_t *P);
  * same stream; calls that overlap on different streams need their own.      */
 nbsgd_status nbsgd_mlp_workspace_bytes(const nbsgd_mlp_shape *s, int64_t rows, size_t *bytes);
 
-/* Local shuffling (Alg. 1/2 initialisation and "shuffle local subset after
- * each epoch"; Sec. 3.2 shuffling bullet).  Learner i owns samples
+/* Local shuffling: each learner reshuffles its own shard at every epoch
+ * boundary (Alg. 1/2 initialisation; Sec. 3.2 shuffling bullet).  Learner i owns samples
  * [shard*i, shard*(i+1)).  Local epoch e permutes its shard by Fisher-Yates
  * from the top (position t swaps with floor(w*(t+1)/2^64), w = Philox4x64-10
  * word 0 at counter (e, i, t, 0) under key (seed, 4)); iteration `step` is
@@ -295,8 +322,8 @@ nbsgd_status nbsgd_mlp_workspace_bytes(const nbsgd_mlp_shape *s, int64_t rows, s
 nbsgd_status nbsgd_minibatch_indices(uint64_t seed, uint64_t step, int32_t n, int32_t m, int32_t b,
                                      int32_t shard, int32_t *idx);
 
-/* Per-mini-batch gradients (Alg. 2 "compute the local stochastic gradient",
- * Sec. 3.2 "compute gradients") of every finished mini-batch, each at its
+/* Per-mini-batch gradients (Alg. 2 mini-batch loop, gradient line; Sec. 3.2,
+ * gradient bullet) of every finished mini-batch, each at its
  * learner's replica:
  *   G[i][j][:] = gradient of the mean cross-entropy of the 32 samples
  *                idx[i][j][:] at parameters X[i], for mask[i*m+j] != 0;

@@ -22,10 +22,14 @@ sum).  Modules:
                  learning-rate scaling, momentum, mix and update (Alg. 2;
                  Sec. 3.2 bullets).
 * ``mlp``      - the end-to-end two-layer MLP workload: forward/backward
-                 per mini-batch, local shuffling (Alg. 1 initialisation).
+                 per mini-batch, local shuffling (Alg. 1 initialisation),
+                 training under any mixing kind.
+* ``workload`` - drivers: a workload description mapped to the oracle's delay
+                 model, mixing matrices and order; column windows of the
+                 seeded inputs; several iterations of the step.
 
 Parity pins for each function live in ``tests/test_oracle_*.py``; functions
 with no pin say "parity unpinned" in their docstring.
 """
 
-from . import mixing, mlp, philox, schedule, step  # noqa: F401
+from . import mixing, mlp, philox, schedule, step, workload  # noqa: F401

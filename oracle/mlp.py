@@ -3,10 +3,10 @@
 The objective is the mean softmax cross-entropy of a 3072 -> 512 (ReLU) -> 10
 network (Eq. 1 with l the per-sample loss).  For each finished mini-batch the
 learner computes the gradient of the mini-batch's mean loss at its own replica
-(Alg. 2, "compute and accumulate the local stochastic gradient").  Local data
+(Alg. 2, gradient line of the mini-batch loop).  Local data
 and sampling follow the initialisation line of Alg. 1/2: the data set is split
 into n equal shards, learner i owns shard i, and the shard is reshuffled at
-the start of every local epoch (Sec. 3.2, "shuffling" bullet).
+the start of every local epoch (Sec. 3.2, shuffling bullet).
 
 Flat parameter layout (the replica rows X[i] of the step): W1[d_in][hidden]
 row-major at 0, b1 at d_in*hidden, W2[hidden][classes] at d_in*hidden+hidden,
@@ -24,6 +24,13 @@ Pins (tests/test_oracle_mlp.py): finite differences and torch.autograd in
 exact mode, the Sec. 5.1 identity (the mean of equal-size mini-batch gradients
 is the joint-batch gradient), bf16 rounding against torch's bfloat16 cast, the
 initial loss near ln(classes), and permutation invariants of the shuffle.
+Pins of ``train`` (tests/test_oracle_mlp_train.py), each against torch
+autograd in float64: with every mini-batch finished and uniform W it is
+synchronous SGD with momentum on the joint batch of the learners' windows
+(Sec. 5.1 with Eq. 2), evaluation losses included; with partial masks and no
+momentum one iteration is SGD on the finished samples only; the first
+mix-then-step iteration is each learner's own SGD step with lr c_i / m; the
+workload's mixing kind is the one applied.
 """
 
 from __future__ import annotations
@@ -150,27 +157,34 @@ class Shuffler:
 
 
 # ------------------------------------------------------------------ training
-def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None, blocking: bool = False):
-    """Non-blocking D-PSGD on the MLP (Alg. 2): every iteration draws the
-    schedule, computes the gradient of each finished mini-batch at the
-    learner's own replica, then mixes and steps with the ring W.
+def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None, blocking: bool = False,
+          evaluate: bool = True, stop=None):
+    """Non-blocking decentralized SGD on the MLP (Alg. 2): every iteration
+    draws the schedule, computes the gradient of each finished mini-batch at
+    the learner's own replica, then mixes and steps with the workload's W
+    (``wl.mixing``: uniform for ring all-reduce, ring for D-PSGD, matcha for
+    MATCHA's random matchings) in the workload's order.
 
-    ``wl`` carries n, m, batch, the shape, delay model, lr, momentum, seed and
-    the evaluation cadence; A[samples][d_in] and y are the data, x0 the common
-    initial replica.  Returns a dict with per-step mean losses (over learners,
-    of the mean over their finished mini-batches), evaluation losses of the
-    average replica (Alg. 1 output) every ``wl.eval_every`` steps and at the
-    end, per-step finished counts, and the final X and V (fp64).
+    ``wl`` carries n, m, batch, the shape, delay model, mixing kind, order,
+    lr, momentum, seed and the evaluation cadence; A[samples][d_in] and y are
+    the data, x0 the common initial replica (Alg. 1/2 initialisation).
+    ``blocking``: the synchronous baseline on the same W and data, every
+    mini-batch finished and each iteration charged the slowest learner's
+    time.  Returns a dict with per-step mean losses (over learners, of the
+    mean over their finished mini-batches), evaluation losses of the average
+    replica (the method's output, Alg. 1/2) every ``wl.eval_every`` steps and
+    at the end (when ``evaluate``), per-step finished counts and simulated
+    seconds, and the final X and V (fp64).  ``stop`` (optional) is called
+    after each iteration with its index and ends training early when it
+    returns True.
     """
-    from . import mixing, schedule, step as step_mod
+    from . import schedule, step as step_mod, workload
 
     s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
     n, m, P = wl.n, wl.m, s.n_params
-    kinds = {"const": schedule.DELAY_CONST, "exp": schedule.DELAY_EXP, "lomax": schedule.DELAY_LOMAX}
-    d = schedule.Delay(kinds[wl.delay.kind], wl.delay.base, wl.delay.param, wl.delay.slow_learner,
-                       wl.delay.slow_factor, wl.delay.slow_prob)
-    W = mixing.w_ring(n).astype(np.float32).astype(np.float64)
-    order = step_mod.MIX_THEN_STEP if wl.order == "mix_then_step" else step_mod.STEP_THEN_MIX
+    d = workload.delay(wl)
+    mixer = workload.mixer(wl)
+    order = workload.order(wl)
     lr, mu = float(np.float32(wl.lr)), float(np.float32(wl.momentum))
     shuf = Shuffler(wl.seed, wl.n_samples // n, m, wl.batch)
     X = np.tile(np.asarray(x0, dtype=np.float64), (n, 1))
@@ -178,7 +192,7 @@ def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None, blocking: bool =
     ev_idx = wl.eval_indices()
     out = dict(step_loss=[], counts=[], eval_step=[], eval_loss=[], seconds=[])
 
-    def evaluate(k):
+    def evaluate_mean(k):
         xbar = X.mean(axis=0)
         losses = [forward(xbar, A[ev_idx[r:r + s.batch]], y[ev_idx[r:r + s.batch]], s, mode)[0]
                   for r in range(0, len(ev_idx), s.batch)]
@@ -186,9 +200,10 @@ def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None, blocking: bool =
         out["eval_loss"].append(float(np.mean(losses)))
 
     G = np.zeros((n, m, P))
+    k = 0
     for k in range(steps):
-        if k % wl.eval_every == 0:
-            evaluate(k)
+        if evaluate and k % wl.eval_every == 0:
+            evaluate_mean(k)
         sch = schedule.sample_schedule(wl.seed, k, n, m, d)
         if blocking:
             sch["mask"] = np.ones((n, m), dtype=np.uint8)
@@ -207,9 +222,16 @@ def train(wl, A, y, x0, steps: int, mode: str = BF16, log=None, blocking: bool =
             learner_losses.append(np.mean(ls))
         out["step_loss"].append(float(np.mean(learner_losses)))
         out["counts"].append(sch["counts"].copy())
-        X, V = step_mod.step(X, V, G, sch["mask"], W, lr, mu, order)
+        X, V = step_mod.step(X, V, G, sch["mask"], mixer.w(k), lr, mu, order)
         if log:
             log(k, out["step_loss"][-1])
-    evaluate(steps)
+        if stop is not None and stop(k):
+            k += 1
+            break
+    else:
+        k = steps
+    if evaluate:
+        evaluate_mean(k)
     out["X"], out["V"] = X, V
+    out["iterations"] = len(out["step_loss"])
     return out

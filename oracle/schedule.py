@@ -3,9 +3,9 @@ the finished-mini-batch mask of one iteration (Alg. 2, the mini-batch loop;
 Lemma 1 and Thm 2 for the timing model).
 
 Each learner processes its N mini-batches in order.  The first learner to
-finish all of them broadcasts the terminal signal (Alg. 2, "broadcast terminal
-signals if n = N"); every learner keeps the mini-batches it finished by then and
-abandons the rest.  With the times of learner i written t[i, 0..m-1] and their
+finish all of them broadcasts the terminal signal (Alg. 2, the branch taken
+when a learner's count reaches N); every learner keeps the mini-batches it
+finished by then and abandons the rest.  With the times of learner i written t[i, 0..m-1] and their
 running sums C[i, j], the signal time is T = min_i C[i, m-1] and learner i keeps
 mini-batches j with C[i, j] <= T (finished by the signal time, boundary
 included).  A learner that finished none keeps its first one (the step is
@@ -115,3 +115,49 @@ def sample_schedule(seed: int, step: int, n: int, m: int, d: Delay) -> dict:
     t_step = max(deadline, max(finish[i, counts[i] - 1] for i in range(n)))
     return dict(times=times, finish=finish, deadline=deadline, counts=counts, mask=mask,
                 t_sync=t_sync, t_step=t_step)
+
+
+def accounting(times) -> dict:
+    """Sec. 4.3 accounting of one iteration from its per-mini-batch times
+    t[n, m] (the schedule's ``times``), in units of mini-batches (the batch
+    B is the m mini-batches of a learner).
+
+    Learner i's time for its whole batch is X_i = sum_j t[i, j] (summed in
+    mini-batch order, as the schedule's running sums); X_{k:P} is the k-th
+    smallest of the X_i, and Y = sum_k 1 / X_{k:P}, summed from the fastest
+    to the slowest learner.  Then:
+
+    * ``throughput``       Thm 3: B * Y, each learner's B / X_i added up;
+    * ``throughput_sync``  Thm 4: P * B / X_{P:P}, the blocking baseline's;
+    * ``data``             Cor. 1: B * Y * X_{1:P}, the (fractional) amount
+                           of data trained in one non-blocking iteration,
+                           which lasts X_{1:P}, when every learner runs at a
+                           constant speed within the iteration;
+    * ``ratio``            Thm 5: Y * X_{P:P} / P, the non-blocking over
+                           the blocking throughput.
+
+    Pins (tests/test_oracle_schedule.py): equal times give Y X_{1:P} = P and a
+    ratio of 1; under constant per-learner speeds (DELAY_CONST with the
+    random slow-down) the schedule's finished counts lie within P of the
+    Cor. 1 amount, below it; the ratio is at least 1 and equals Thm 3 over
+    Thm 4.
+    """
+    times = np.asarray(times, dtype=np.float64)
+    n, m = times.shape
+    X = []
+    for i in range(n):
+        total = 0.0
+        for j in range(m):
+            total = total + float(times[i, j])
+        if not total > 0.0:
+            raise ValueError(f"learner {i} has a non-positive batch time")
+        X.append(total)
+    order_stats = sorted(X)
+    Y = 0.0
+    for x in order_stats:
+        Y = Y + 1.0 / x
+    x_first, x_last = order_stats[0], order_stats[-1]
+    throughput = m * Y
+    return dict(x_first=x_first, x_last=x_last, y=Y, throughput=throughput,
+                throughput_sync=(n * m) / x_last, data=throughput * x_first,
+                ratio=(Y * x_last) / n)

@@ -1,6 +1,6 @@
 """One Non-blocking iteration on n learner replicas (Alg. 2, averaging and
-update steps; Sec. 3.2, "adjust learning rate", "compute gradients",
-"averaging" and "gradient update" bullets), plus heavy-ball momentum.
+update steps; Sec. 3.2, the learning-rate, gradient, averaging and update
+bullets), plus heavy-ball momentum.
 
 Shapes: X[n, P] replicas, V[n, P] momentum buffers, G[n, m, P] per-mini-batch
 gradients, mask[n, m] (nonzero = finished before the terminal signal),

@@ -13,6 +13,7 @@ from ._lib import (  # noqa: F401
     Matcha,
     NbsgdError,
     accumulate,
+    iteration_accounting,
     load,
     minibatch_indices,
     mix,

@@ -23,13 +23,14 @@ DELAY_CONST, DELAY_EXP, DELAY_LOMAX = 0, 1, 2
 MAX_LEARNERS, MAX_MINIBATCHES = 16, 64
 SLOW_NONE, SLOW_RANDOM = -1, -2
 
-EXPORTS = ("nbsgd_sample_mask", "nbsgd_accumulate", "nbsgd_mix", "nbsgd_update", "nbsgd_step",
+EXPORTS = ("nbsgd_sample_mask", "nbsgd_iteration_accounting", "nbsgd_accumulate", "nbsgd_mix", "nbsgd_update", "nbsgd_step",
            "nbsgd_step_strided", "nbsgd_row_stride",
            "nbsgd_w_allreduce", "nbsgd_w_ring", "nbsgd_matcha_create", "nbsgd_matcha_w",
            "nbsgd_matcha_matchings", "nbsgd_matcha_set", "nbsgd_matcha_get", "nbsgd_matcha_optimize",
            "nbsgd_matcha_destroy", "nbsgd_mlp_param_count",
            "nbsgd_mlp_workspace_bytes", "nbsgd_minibatch_indices", "nbsgd_mlp_grad",
-           "nbsgd_mlp_grad_strided", "nbsgd_mlp_loss", "nbsgd_last_error")
+           "nbsgd_mlp_grad_strided", "nbsgd_mlp_loss",
+           "nbsgd_last_error")
 
 
 class NbsgdError(RuntimeError):
@@ -49,6 +50,11 @@ class Delay(ctypes.Structure):
                 ("slow_prob", ctypes.c_double)]
 
 
+class Accounting(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_double) for k in ("x_first", "x_last", "y", "throughput",
+                                                 "throughput_sync", "data", "ratio")]
+
+
 _c_void_p, _i32, _i64, _u64, _f32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
                                      ctypes.c_uint64, ctypes.c_float)
 _lib = None
@@ -64,6 +70,7 @@ def load():
     sig = {
         "nbsgd_sample_mask": [_u64, _u64, _i32, _i32, ctypes.POINTER(Delay), _c_void_p, _c_void_p,
                               _c_void_p, _c_void_p],
+        "nbsgd_iteration_accounting": [_c_void_p, _i32, _i32, ctypes.POINTER(Accounting)],
         "nbsgd_accumulate": [_c_void_p, _c_void_p, _i32, _i32, _i64, _c_void_p, _c_void_p],
         "nbsgd_mix": [_c_void_p, _c_void_p, _i32, _i64, _c_void_p, _c_void_p],
         "nbsgd_update": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i64, _f32, _f32,
@@ -161,6 +168,18 @@ def sample_mask(seed: int, step: int, n: int, m: int, kind: int, base: float = 1
     _check(load().nbsgd_sample_mask(seed, step, n, m, ctypes.byref(d), _host_ptr(mask),
                                     _host_ptr(counts), _host_ptr(times), _host_ptr(timing)))
     return mask, counts, times, timing
+
+
+def iteration_accounting(times) -> dict:
+    """Sec. 4.3 accounting (Thm 3-5, Cor. 1) of one iteration's per-mini-batch
+    times [n, m]; returns the fields of nbsgd_accounting as a dict."""
+    times = np.ascontiguousarray(np.asarray(times), dtype=np.float64)
+    if times.ndim != 2:
+        raise ValueError("times must be [n, m]")
+    n, m = times.shape
+    a = Accounting()
+    _check(load().nbsgd_iteration_accounting(_host_ptr(times), n, m, ctypes.byref(a)))
+    return {k: getattr(a, k) for k, _ in Accounting._fields_}
 
 
 def w_allreduce(n: int) -> np.ndarray:

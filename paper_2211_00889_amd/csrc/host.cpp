@@ -166,6 +166,38 @@ extern "C" nbsgd_status nbsgd_sample_mask(uint64_t seed, uint64_t step, int32_t 
   return NBSGD_OK;
 }
 
+// --------------------------------------------------- Sec. 4.3 accounting
+extern "C" nbsgd_status nbsgd_iteration_accounting(const double* times, int32_t n, int32_t m,
+                                                   nbsgd_accounting* out) {
+  clear_error();
+  if (nbsgd_status st = check_nm(n, m)) return st;
+  if (!times || !out) return fail(NBSGD_E_ARG, "times and out must not be null");
+  double X[NBSGD_MAX_LEARNERS];
+  for (int32_t i = 0; i < n; ++i) {
+    double total = 0.0;
+    for (int32_t j = 0; j < m; ++j) {
+      const double t = times[i * m + j];
+      if (!isfinite(t) || t < 0.0)
+        return fail(NBSGD_E_ARG, "times[%d][%d]=%g is negative or not finite", i, j, t);
+      total = total + t;
+    }
+    if (!(total > 0.0)) return fail(NBSGD_E_ARG, "learner %d's batch time is not positive", i);
+    X[i] = total;
+  }
+  // order statistics X_{1:P} <= ... <= X_{P:P}; Y summed from the fastest
+  std::sort(X, X + n);
+  double Y = 0.0;
+  for (int32_t k = 0; k < n; ++k) Y = Y + 1.0 / X[k];
+  out->x_first = X[0];
+  out->x_last = X[n - 1];
+  out->y = Y;
+  out->throughput = (double)m * Y;
+  out->throughput_sync = (double)((int64_t)n * m) / X[n - 1];
+  out->data = out->throughput * X[0];
+  out->ratio = (Y * X[n - 1]) / (double)n;
+  return NBSGD_OK;
+}
+
 // --------------------------------------------------------- mixing matrices
 extern "C" nbsgd_status nbsgd_w_allreduce(int32_t n, float* W) {
   clear_error();

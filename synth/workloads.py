@@ -105,6 +105,8 @@ class MlpWorkload:
     eval_every: int = 10
     eval_samples: int = 4096
     eval_stride: int = 12      # evaluation subset: samples 0, 12, 24, ...
+    matcha_degree: int = 3
+    matcha_budget: float | None = None
 
     @property
     def P(self) -> int:

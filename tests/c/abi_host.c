@@ -49,7 +49,15 @@ static void schedule(void) {
     }
     CHECK(full); /* the learner that sent the terminal signal finished all m */
     CHECK(timing[0] <= timing[2] && timing[2] <= timing[1]);
+    /* Sec. 4.3 accounting: X_{1:P} and X_{P:P} are the two iteration times,
+     * Thm 5 is Thm 3 over Thm 4 and at least 1 */
+    nbsgd_accounting a;
+    CHECK(nbsgd_iteration_accounting(times, n, m, &a) == NBSGD_OK);
+    CHECK(a.x_first == timing[0] && a.x_last == timing[1]);
+    CHECK(a.ratio >= 1.0 && fabs(a.ratio - a.throughput / a.throughput_sync) < 1e-12 * a.ratio);
+    CHECK(a.data >= m - 1e-9 && a.data <= n * m + 1e-9);
   }
+  CHECK(nbsgd_iteration_accounting(NULL, n, m, NULL) == NBSGD_E_ARG);
   /* constant delays: everybody finishes everything */
   nbsgd_delay c = {NBSGD_DELAY_CONST, 1.0, 0.0, -1, 1.0, 0.0};
   CHECK(nbsgd_sample_mask(3, 0, n, m, &c, mask, counts, NULL, NULL) == NBSGD_OK);

@@ -48,3 +48,26 @@ def test_committed_traffic_records_are_consistent(path):
     assert rec["traffic_over_alg"] == pytest.approx(ratio, rel=1e-12)
     assert abs(ratio - 1.0) < 0.01
     assert rec["workload"] in os.path.basename(path)
+
+
+def test_bench_imports_nothing_from_the_test_package():
+    src = open(os.path.join(ROOT, "bench.py")).read()
+    assert "tests." not in src and "from tests" not in src and "import tests" not in src
+
+
+def test_cpu_baselines_run_on_the_oracle():
+    """Both CPU-baseline legs on small workloads, with a tiny time budget:
+    whole oracle iterations, the rate in the bench's units."""
+    from synth import workloads
+
+    r = bench.cpu_baseline(workloads.TINY, budget_s=0.2, cols=4096)
+    assert r["kind"] == "oracle" and r["cores"] == 1 and r["value"] > 0
+    assert "columns [0, 4096)" in r["sample"]
+    from synth import mlp_data
+
+    wl = workloads.MLP_TINY
+    A = mlp_data.inputs(wl.seed, wl.n_samples, wl.d_in)
+    y = mlp_data.teacher_labels(wl.seed, A, wl.hidden, wl.classes)
+    x0 = mlp_data.student_init(wl.seed, wl.d_in, wl.hidden, wl.classes)
+    r = bench.cpu_baseline_mlp(wl, A, y, x0, budget_s=0.2)
+    assert r["unit"] == "samples/s" and r["value"] > 0 and "iterations 0.." in r["sample"]

@@ -300,3 +300,42 @@ def test_row_stride_rule():
         nb._lib.row_stride(-1)
     assert e.value.status == _lib.E_SHAPE
     assert _lib.load().nbsgd_row_stride(5, None) == _lib.E_ARG
+
+
+@pytest.mark.parametrize("delay", DELAYS)
+@pytest.mark.parametrize("n,m", [(1, 1), (4, 4), (8, 8), (16, 4), (3, 64)])
+def test_iteration_accounting_bitwise(delay, n, m):
+    """Thm 3-5 / Cor. 1 accounting: the library's fp64 figures equal the
+    oracle's bit for bit (same sums in the same order)."""
+    kind, base, param, slow, factor, prob = delay
+    if slow >= n:
+        slow = n - 1
+    if base == 0.0 and kind == nb.DELAY_CONST:
+        return
+    for seed, step in ((0, 0), (5, 17)):
+        _, _, times, timing = nb.sample_mask(seed, step, n, m, kind, base, param, slow, factor, prob)
+        got = nb.iteration_accounting(times)
+        want = oracle.schedule.accounting(times)
+        assert got == want
+        assert got["x_first"] == timing[0] and got["x_last"] == timing[1]
+
+
+def test_iteration_accounting_errors():
+    lib = _lib.load()
+    a = _lib.Accounting()
+    t = np.ones((2, 3))
+    assert lib.nbsgd_iteration_accounting(None, 2, 3, ctypes.byref(a)) == _lib.E_ARG
+    assert lib.nbsgd_iteration_accounting(t.ctypes.data_as(ctypes.c_void_p), 2, 3, None) == _lib.E_ARG
+    for bad in (-1.0, float("nan"), float("inf")):
+        t[1, 2] = bad
+        assert lib.nbsgd_iteration_accounting(t.ctypes.data_as(ctypes.c_void_p), 2, 3,
+                                              ctypes.byref(a)) == _lib.E_ARG
+    t = np.ones((2, 3))
+    t[0] = 0.0
+    assert lib.nbsgd_iteration_accounting(t.ctypes.data_as(ctypes.c_void_p), 2, 3,
+                                          ctypes.byref(a)) == _lib.E_ARG
+    assert b"learner 0" in lib.nbsgd_last_error()
+    assert lib.nbsgd_iteration_accounting(t.ctypes.data_as(ctypes.c_void_p), 0, 3,
+                                          ctypes.byref(a)) == _lib.E_SHAPE
+    assert lib.nbsgd_iteration_accounting(t.ctypes.data_as(ctypes.c_void_p), 17, 3,
+                                          ctypes.byref(a)) == _lib.E_UNSUPPORTED

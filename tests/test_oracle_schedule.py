@@ -120,3 +120,56 @@ def test_random_slowdown_model():
     sch = schedule.sample_schedule(3, 5, 8, 4, d)
     np.testing.assert_array_equal(sch["times"][:, 0], scales[5])
     assert sch["times"].max() / sch["times"].min() < 2.0
+
+
+# ------------------------------------------------ Sec. 4.3 accounting (Thm 3-5, Cor. 1)
+@pytest.mark.parametrize("n,m", [(1, 1), (4, 4), (8, 8), (16, 4)])
+def test_accounting_equal_times(n, m):
+    """Every learner as fast as the others: Y X_{1:P} = P, the Cor. 1 amount
+    is the whole P B, and non-blocking has the blocking throughput (Thm 5 ratio
+    1)."""
+    s = schedule.sample_schedule(0, 3, n, m, Delay(DELAY_CONST, 1.5, 0.0))
+    a = schedule.accounting(s["times"])
+    assert a["x_first"] == a["x_last"] == 1.5 * m
+    assert a["y"] * a["x_first"] == pytest.approx(n, rel=1e-15)
+    assert a["data"] == pytest.approx(n * m, rel=1e-15)
+    assert a["ratio"] == pytest.approx(1.0, rel=1e-15)
+    assert a["throughput"] == pytest.approx(a["throughput_sync"], rel=1e-15)
+
+
+@pytest.mark.parametrize("n,m,factor", [(8, 8, 2.0), (16, 4, 2.0), (5, 64, 3.0), (8, 16, 1.3)])
+def test_accounting_constant_speed_bounds_finished_counts(n, m, factor):
+    """Cor. 1 assumes each learner runs at a constant speed within the
+    iteration.  DELAY_CONST with the random slow-down is exactly that (learner
+    i's mini-batches all take s_i), so learner i finishes floor(m T / X_i) of
+    them by T = X_{1:P}: the finished total lies in (data - P, data]."""
+    d = Delay(DELAY_CONST, 1.0, 0.0, schedule.SLOW_RANDOM, factor, 0.5)
+    for step in range(40):
+        s = schedule.sample_schedule(11, step, n, m, d)
+        a = schedule.accounting(s["times"])
+        total = int(s["counts"].sum())
+        assert a["data"] - n - 1e-9 < total <= a["data"] + 1e-9, step
+        assert a["x_first"] == s["deadline"] and a["x_last"] == s["t_sync"]
+        X = s["finish"][:, m - 1]
+        for i in range(n):
+            share = m * a["x_first"] / X[i]  # learner i's Cor. 1 share
+            assert share - 1 - 1e-9 < s["counts"][i] <= share + 1e-9, (step, i)
+
+
+@pytest.mark.parametrize("kind,param,slow,factor", [(DELAY_EXP, 1.0, -1, 1.0), (DELAY_LOMAX, 1.5, -1, 1.0),
+                                                    (DELAY_EXP, 1.0, 7, 3.0)])
+def test_accounting_invariants(kind, param, slow, factor):
+    """Thm 5 is Thm 3 over Thm 4, at least 1 (no learner is slower than the
+    slowest), and Y X_{1:P} lies between 1 (the fastest learner's own share)
+    and P."""
+    n, m = 8, 8
+    for step in range(30):
+        s = schedule.sample_schedule(2, step, n, m, Delay(kind, 1.0, param, slow, factor))
+        a = schedule.accounting(s["times"])
+        assert a["ratio"] == pytest.approx(a["throughput"] / a["throughput_sync"], rel=1e-14)
+        assert a["ratio"] >= 1.0 - 1e-15
+        yx = a["data"] / m
+        assert 1.0 - 1e-12 <= yx <= n + 1e-12
+        # Y itself: the per-learner throughputs added up, in any order
+        X = s["finish"][:, m - 1]
+        assert a["y"] == pytest.approx(float(np.sum(1.0 / X)), rel=1e-14)
