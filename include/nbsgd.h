@@ -361,6 +361,30 @@ nbsgd_status nbsgd_mlp_grad_strided(const float *X, int64_t ld, int32_t n, int32
                                     const uint8_t *mask, float *G, float *losses, void *workspace,
                                     size_t workspace_bytes, void *stream);
 
+/* Allocation-free nbsgd_mlp_grad_strided, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same kernels and results, bit for bit, with the
+ * workspace taken from a static device buffer of NBSGD_MLP_SCRATCH_BYTES
+ * (32 MiB) that every GPU the library is loaded on holds until the process
+ * ends.  Nothing is allocated or freed; the buffer's device address is looked
+ * up once per device (hipGetSymbolAddress, with that device current).
+ * The finished mini-batches' workspace, min(finished, 896) * batch rows of
+ * nbsgd_mlp_workspace_bytes, must fit the buffer (NBSGD_E_UNSUPPORTED
+ * otherwise, before anything is enqueued): up to 113 finished mini-batches
+ * of a 512-unit hidden layer, e.g. every mini-batch of n = 8, m = 8 (64).
+ * The kernels write every byte of the buffer they later read, so nothing is
+ * cleared between calls.  All calls on one GPU share its buffer: calls that
+ * overlap on that GPU (other streams, other host threads) race; calls on one
+ * stream run in order.  `stream` must belong to the current device
+ * (NBSGD_E_ARG).  Arguments and layout as nbsgd_mlp_grad_strided.
+ * Errors: as nbsgd_mlp_grad_strided, and NBSGD_E_UNSUPPORTED (too many
+ * finished mini-batches for the buffer, or a device index above 63).        */
+#define NBSGD_MLP_SCRATCH_BYTES (32u * 1024u * 1024u)
+nbsgd_status nbsgd_mlp_grad_noalloc(const float *X, int64_t ld, int32_t n, int32_t m,
+                                    const nbsgd_mlp_shape *s, const float *data,
+                                    const int32_t *labels, int64_t n_samples, const int32_t *idx,
+                                    const uint8_t *mask, float *G, float *losses, void *stream);
+
 /* Mean cross-entropy of one parameter vector on `count` samples, in batches
  * of 32: losses[k] = mean loss of samples idx[32k .. 32k+31] (same precision
  * as nbsgd_mlp_grad's forward pass).  Used to evaluate the average of the

@@ -18,6 +18,7 @@ from ._lib import (  # noqa: F401
     minibatch_indices,
     mix,
     mlp_grad,
+    mlp_grad_noalloc,
     mlp_grad_strided,
     mlp_loss,
     mlp_param_count,

@@ -29,7 +29,7 @@ EXPORTS = ("nbsgd_sample_mask", "nbsgd_iteration_accounting", "nbsgd_accumulate"
            "nbsgd_matcha_matchings", "nbsgd_matcha_set", "nbsgd_matcha_get", "nbsgd_matcha_optimize",
            "nbsgd_matcha_destroy", "nbsgd_mlp_param_count",
            "nbsgd_mlp_workspace_bytes", "nbsgd_minibatch_indices", "nbsgd_mlp_grad",
-           "nbsgd_mlp_grad_strided", "nbsgd_mlp_loss",
+           "nbsgd_mlp_grad_strided", "nbsgd_mlp_grad_noalloc", "nbsgd_mlp_loss",
            "nbsgd_last_error")
 
 
@@ -97,6 +97,9 @@ def load():
         "nbsgd_mlp_grad_strided": [_c_void_p, _i64, _i32, _i32, ctypes.POINTER(MlpShape), _c_void_p,
                                    _c_void_p, _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                    _c_void_p, ctypes.c_size_t, _c_void_p],
+        "nbsgd_mlp_grad_noalloc": [_c_void_p, _i64, _i32, _i32, ctypes.POINTER(MlpShape), _c_void_p,
+                                   _c_void_p, _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                   _c_void_p],
         "nbsgd_mlp_loss": [_c_void_p, ctypes.POINTER(MlpShape), _c_void_p, _c_void_p, _i64, _c_void_p,
                            _i32, _c_void_p, _c_void_p, ctypes.c_size_t, _c_void_p],
     }
@@ -377,6 +380,20 @@ def mlp_grad_strided(X, m: int, dims, data, labels, idx, mask, G, losses, worksp
                                          _dev(data, "data"), _i32_dev(labels, "labels"),
                                          data.shape[0], _host_ptr(idx), _host_ptr(mask), _dev(G, "G"),
                                          _dev(losses, "losses"), ws, ws_bytes, _stream(X, stream)))
+
+
+def mlp_grad_noalloc(X, m: int, dims, data, labels, idx, mask, G, losses, stream=None):
+    """nbsgd_mlp_grad_noalloc: mlp_grad_strided with the library's static
+    device scratch buffer as the workspace (no workspace argument)."""
+    ld = X.shape[-1]
+    n, idx, mask = _mlp_grad_args(X, m, dims, data, labels, idx, mask, G, losses, ld)
+    _check(load().nbsgd_mlp_grad_noalloc(_dev(X, "X"), ld, n, m, ctypes.byref(_shape(*dims)),
+                                         _dev(data, "data"), _i32_dev(labels, "labels"),
+                                         data.shape[0], _host_ptr(idx), _host_ptr(mask), _dev(G, "G"),
+                                         _dev(losses, "losses"), _stream(X, stream)))
+
+
+MLP_SCRATCH_BYTES = 32 * 1024 * 1024
 
 
 def mlp_loss(params, dims, data, labels, idx, losses, workspace, stream=None):

@@ -26,6 +26,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "internal.h"
@@ -727,33 +728,38 @@ extern "C" nbsgd_status nbsgd_mlp_workspace_bytes(const nbsgd_mlp_shape* s, int6
 
 namespace {
 
-nbsgd_status mlp_grad_impl(const float* X, int64_t ld, int32_t n, int32_t m,
-                           const nbsgd_mlp_shape* s, const float* data, const int32_t* labels,
-                           int64_t n_samples, const int32_t* idx, const uint8_t* mask, float* G,
-                           float* losses, void* workspace, size_t workspace_bytes, void* stream) {
+// Argument checks shared by the gradient entry points, before the workspace
+// and the sample indices (checked by the caller, in that order): shapes, row
+// stride, pointers and alignment.  On success *d holds the shape with d->ld
+// set and *finished the finished (learner * m + mini-batch) entries in order.
+nbsgd_status mlp_grad_check(const float* X, int64_t ld, int32_t n, int32_t m,
+                            const nbsgd_mlp_shape* s, const float* data, const int32_t* labels,
+                            int64_t n_samples, const int32_t* idx, const uint8_t* mask, float* G,
+                            float* losses, Dims* d, std::vector<int32_t>* finished) {
   if (nbsgd_status st = check_nm(n, m)) return st;
-  Dims d;
-  if (nbsgd_status st = check_shape(s, &d)) return st;
-  if (ld == 0) ld = d.P;
-  if (ld < d.P || ld % 4)
+  if (nbsgd_status st = check_shape(s, d)) return st;
+  if (ld == 0) ld = d->P;
+  if (ld < d->P || ld % 4)
     return fail(NBSGD_E_SHAPE, "row stride %lld must be a multiple of 4 and at least P=%lld",
-                (long long)ld, (long long)d.P);
-  d.ld = ld;
-  if (!X || !data || !labels || !idx || !mask || !G || !losses || !workspace)
+                (long long)ld, (long long)d->P);
+  d->ld = ld;
+  if (!X || !data || !labels || !idx || !mask || !G || !losses)
     return fail(NBSGD_E_ARG, "null pointer argument");
-  if (((uintptr_t)X | (uintptr_t)data | (uintptr_t)G | (uintptr_t)workspace) & 15)
-    return fail(NBSGD_E_ALIGN, "X, data, G and workspace must be 16-byte aligned");
+  if (((uintptr_t)X | (uintptr_t)data | (uintptr_t)G) & 15)
+    return fail(NBSGD_E_ALIGN, "X, data and G must be 16-byte aligned");
   if (n_samples < 1) return fail(NBSGD_E_SHAPE, "n_samples must be >= 1");
-  const int64_t rows = (int64_t)n * m * kBatch;
-  if (workspace_bytes < workspace_for(d, rows))
-    return fail(NBSGD_E_ARG, "workspace of %zu bytes is below the %zu needed", workspace_bytes,
-                workspace_for(d, rows));
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const Workspace w = carve(workspace, d, rows);
-  std::vector<int32_t> finished;
+  finished->clear();
   for (int32_t k = 0; k < n * m; ++k)
-    if (mask[k]) finished.push_back(k);
-  if (nbsgd_status r = check_idx(idx, finished.data(), (int)finished.size(), n_samples)) return r;
+    if (mask[k]) finished->push_back(k);
+  return NBSGD_OK;
+}
+
+// Launches the gradient kernels of the finished mini-batches in groups of at
+// most kMaxList, each group's workspace rows starting at entry 0 of `w`.
+nbsgd_status mlp_grad_launch(const float* X, int32_t m, const Dims& d, const float* data,
+                             const int32_t* labels, int64_t n_samples, const int32_t* idx,
+                             const std::vector<int32_t>& finished, float* G, float* losses,
+                             const Workspace& w, hipStream_t st) {
   const bool wide = n_samples > 65536;
   std::pair<int, int> mb[kMaxList];
   int count = 0;
@@ -766,6 +772,67 @@ nbsgd_status mlp_grad_impl(const float* X, int64_t ld, int32_t n, int32_t m,
   }
   if (count) launch_group<true>(mb, count, idx, wide, X, data, labels, w, G, losses, d, st);
   return launch_err("nbsgd_mlp_grad");
+}
+
+nbsgd_status mlp_grad_impl(const float* X, int64_t ld, int32_t n, int32_t m,
+                           const nbsgd_mlp_shape* s, const float* data, const int32_t* labels,
+                           int64_t n_samples, const int32_t* idx, const uint8_t* mask, float* G,
+                           float* losses, void* workspace, size_t workspace_bytes, void* stream) {
+  Dims d;
+  std::vector<int32_t> finished;
+  if (nbsgd_status st = mlp_grad_check(X, ld, n, m, s, data, labels, n_samples, idx, mask, G,
+                                       losses, &d, &finished))
+    return st;
+  if (!workspace) return fail(NBSGD_E_ARG, "null pointer argument");
+  if ((uintptr_t)workspace & 15) return fail(NBSGD_E_ALIGN, "workspace must be 16-byte aligned");
+  const int64_t rows = (int64_t)n * m * kBatch;
+  if (workspace_bytes < workspace_for(d, rows))
+    return fail(NBSGD_E_ARG, "workspace of %zu bytes is below the %zu needed", workspace_bytes,
+                workspace_for(d, rows));
+  if (nbsgd_status r = check_idx(idx, finished.data(), (int)finished.size(), n_samples)) return r;
+  return mlp_grad_launch(X, m, d, data, labels, n_samples, idx, finished, G, losses,
+                         carve(workspace, d, rows), reinterpret_cast<hipStream_t>(stream));
+}
+
+// ------------------------------------------------ allocation-free variant
+// The workspace of nbsgd_mlp_grad_noalloc: a static device array, one copy
+// per GPU the library is loaded on, held until the process ends.  Host code
+// never passes `scratch` itself to a kernel (on the host the name is only a
+// stand-in for the symbol): the device address of each GPU's copy comes from
+// hipGetSymbolAddress with that GPU current, and is kept per device.
+static __device__ __align__(256) unsigned char scratch[NBSGD_MLP_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch, looked up once per device.
+nbsgd_status scratch_address(hipStream_t stream, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(NBSGD_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (stream) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return fail(NBSGD_E_HIP, "hipStreamGetDevice: %s", hipGetErrorString(e));
+    if (sdev != dev)
+      return fail(NBSGD_E_ARG, "stream belongs to device %d but device %d is current", (int)sdev,
+                  dev);
+  }
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(NBSGD_E_UNSUPPORTED, "device %d is beyond the %d devices supported", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(NBSGD_E_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                  hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return NBSGD_OK;
 }
 
 }  // namespace
@@ -790,6 +857,35 @@ extern "C" nbsgd_status nbsgd_mlp_grad_strided(const float* X, int64_t ld, int32
   if (ld <= 0) return fail(NBSGD_E_SHAPE, "row stride %lld must be positive", (long long)ld);
   return mlp_grad_impl(X, ld, n, m, s, data, labels, n_samples, idx, mask, G, losses, workspace,
                        workspace_bytes, stream);
+}
+
+extern "C" nbsgd_status nbsgd_mlp_grad_noalloc(const float* X, int64_t ld, int32_t n, int32_t m,
+                                               const nbsgd_mlp_shape* s, const float* data,
+                                               const int32_t* labels, int64_t n_samples,
+                                               const int32_t* idx, const uint8_t* mask, float* G,
+                                               float* losses, void* stream) {
+  clear_error();
+  if (ld <= 0) return fail(NBSGD_E_SHAPE, "row stride %lld must be positive", (long long)ld);
+  Dims d;
+  std::vector<int32_t> finished;
+  if (nbsgd_status st = mlp_grad_check(X, ld, n, m, s, data, labels, n_samples, idx, mask, G,
+                                       losses, &d, &finished))
+    return st;
+  // workspace rows for one launch group: the kernels index them by the
+  // group's list entries, so the largest group sets the size
+  const int64_t rows = (int64_t)std::min<size_t>(finished.size(), kMaxList) * kBatch;
+  const size_t need = workspace_for(d, rows);
+  if (need > (size_t)NBSGD_MLP_SCRATCH_BYTES)
+    return fail(NBSGD_E_UNSUPPORTED,
+                "%zu finished mini-batches of this shape need %zu bytes of workspace, above the "
+                "%zu-byte static scratch buffer (use nbsgd_mlp_grad_strided with a workspace)",
+                finished.size(), need, (size_t)NBSGD_MLP_SCRATCH_BYTES);
+  if (nbsgd_status r = check_idx(idx, finished.data(), (int)finished.size(), n_samples)) return r;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  if (nbsgd_status r = scratch_address(st, &ws)) return r;
+  return mlp_grad_launch(X, m, d, data, labels, n_samples, idx, finished, G, losses,
+                         carve(ws, d, rows), st);
 }
 
 extern "C" nbsgd_status nbsgd_mlp_loss(const float* params, const nbsgd_mlp_shape* s,

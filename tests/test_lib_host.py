@@ -302,6 +302,37 @@ def test_row_stride_rule():
     assert _lib.load().nbsgd_row_stride(5, None) == _lib.E_ARG
 
 
+def test_mlp_grad_noalloc_host_checks_before_launch():
+    """The allocation-free gradient call refuses, on the host and before any
+    HIP call (fake device pointers), a request whose workspace exceeds its
+    static buffer, then checks the sample list; a request that fits gets as
+    far as the sample-index check."""
+    lib = _lib.load()
+    shape = _lib.MlpShape(128, 512, 10, 32)
+    n, m = 16, 8
+    idx = np.zeros(n * m * 32, np.int32)
+    mask = np.ones(n * m, np.uint8)
+    p = ctypes.c_void_p(0x100000)
+    P = _lib.mlp_param_count(128, 512, 10)
+
+    def call(mask, ld=P):
+        return lib.nbsgd_mlp_grad_noalloc(p, ld, n, m, ctypes.byref(shape), p, p, 100,
+                                          idx.ctypes.data_as(ctypes.c_void_p),
+                                          mask.ctypes.data_as(ctypes.c_void_p), p, p, None)
+
+    assert _lib.mlp_workspace_bytes(128, 512, 10, 114 * 32) > _lib.MLP_SCRATCH_BYTES
+    assert _lib.mlp_workspace_bytes(128, 512, 10, 113 * 32) <= _lib.MLP_SCRATCH_BYTES
+    assert call(mask) == _lib.E_UNSUPPORTED and b"static scratch" in lib.nbsgd_last_error()
+    few = mask.copy()
+    few[114:] = 0
+    assert call(few) == _lib.E_UNSUPPORTED
+    few[113:] = 0
+    idx[7] = 100  # out of range for n_samples = 100: the next check
+    assert call(few) == _lib.E_ARG and b"position 7" in lib.nbsgd_last_error()
+    assert call(few, ld=P + 2) == _lib.E_SHAPE and b"row stride" in lib.nbsgd_last_error()
+    assert call(few, ld=0) == _lib.E_SHAPE
+
+
 @pytest.mark.parametrize("delay", DELAYS)
 @pytest.mark.parametrize("n,m", [(1, 1), (4, 4), (8, 8), (16, 4), (3, 64)])
 def test_iteration_accounting_bitwise(delay, n, m):
