@@ -114,7 +114,7 @@ class MlpRunner:
     """The end-to-end workload on a device: synthetic data and labels, n
     identical initial replicas, and per iteration the schedule, the shuffled
     mini-batch indices, the per-mini-batch gradients (bf16 MFMA) and the fused
-    step."""
+    step with the workload's mixing kind (ring, MATCHA or uniform W)."""
 
     def __init__(self, wl, device="cuda:0", data=None, labels=None, x0=None):
         import torch
@@ -152,8 +152,9 @@ class MlpRunner:
         ws = _lib.mlp_workspace_bytes(*self.dims, rows)
         self.workspace = torch.empty((ws + 15) // 16 * 4, dtype=torch.float32, device=dev)
         self.mean = torch.zeros_like(self.Xrows)
-        self.mixer = Mixer(wl.mixing, wl.n, wl.seed)
+        self.mixer = Mixer(wl.mixing, wl.n, wl.seed, wl.matcha_degree, wl.matcha_budget)
         self.schedule = Schedule(wl)
+        self.last_schedule = None
         self.order = _ORDER[wl.order]
         self.w_mean = _lib.w_allreduce(wl.n)
 
@@ -163,12 +164,16 @@ class MlpRunner:
         (Alg. 2): the schedule's mask, time T_step (the terminal signal, or a
         forced first mini-batch if later).  ``blocking``: the D-PSGD baseline
         on the same W, every learner finishes all m mini-batches and the
-        iteration waits for the slowest, T_sync.  The finished mini-batches'
-        losses are left in ``self.losses`` (index i*m + j).  ``events``: a
-        list that receives three recorded device events (before the
-        gradients, between gradients and step, after the step)."""
+        iteration waits for the slowest, T_sync (the synchronous baseline of
+        the workload's mixing kind: D-PSGD, MATCHA or all-reduce).  The
+        finished mini-batches' losses are left in ``self.losses`` (index i*m +
+        j).  ``events``: a list that receives three recorded device events
+        (before the gradients, between gradients and step, after the step).
+        The iteration's schedule (mask, counts, per-mini-batch times, timing)
+        is kept in ``last_schedule``."""
         wl = self.wl
-        mask, counts, _, timing = self.schedule.mask(k)
+        mask, counts, times, timing = self.schedule.mask(k)
+        self.last_schedule = (mask, counts, times, timing)
         seconds = float(timing[2])
         if blocking:
             mask = np.ones_like(mask)

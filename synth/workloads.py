@@ -133,3 +133,17 @@ MLP_TINY = MlpWorkload("mlp_tiny_n4_m4_b32_128x64x10_ring", n=4, m=4, d_in=128, 
 MLP_HETERO = replace(MLP, name="mlp_n8_m8_b32_3072x512x10_ring_random_slowdown",
                      delay=DelaySpec("const", 1.0, 0.0, slow_learner=-2, slow_factor=2.0,
                                      slow_prob=0.5))
+
+
+# The three mixing kinds the paper compares (Sec. 6.2): D-PSGD on the ring
+# (above), MATCHA's random matchings of a 3-regular base graph (budget 0.5)
+# and ring all-reduce, i.e. uniform W, stepping before the average (Eq. 4-5).
+MIXINGS = {"ring": dict(mixing="ring", order=MIX_THEN_STEP),
+           "matcha": dict(mixing="matcha", order=MIX_THEN_STEP),
+           "uniform": dict(mixing="uniform", order=STEP_THEN_MIX)}
+
+
+def mlp_with_mixing(wl: MlpWorkload, kind: str) -> MlpWorkload:
+    """The MLP workload ``wl`` with another mixing kind (and its order)."""
+    name = wl.name.replace("_ring", f"_{'allreduce' if kind == 'uniform' else kind}")
+    return replace(wl, name=name, **MIXINGS[kind])

@@ -20,3 +20,17 @@ def test_time_to_takes_the_first_crossing():
     times = [0.0, 1.0, 2.0, 3.0]
     losses = [1.0, 0.4, 0.8, 0.2]
     assert time_to(times, losses, 0.5) == pytest.approx(0.5 / 0.6)  # between evaluations 0 and 1
+
+
+def test_mlp_workloads_of_each_mixing_kind():
+    from synth import workloads
+
+    for base in (workloads.MLP, workloads.MLP_HETERO):
+        ring = workloads.mlp_with_mixing(base, "ring")
+        assert ring == base
+        m = workloads.mlp_with_mixing(base, "matcha")
+        u = workloads.mlp_with_mixing(base, "uniform")
+        assert (m.mixing, m.order) == ("matcha", workloads.MIX_THEN_STEP) and "_matcha" in m.name
+        assert (u.mixing, u.order) == ("uniform", workloads.STEP_THEN_MIX) and "_allreduce" in u.name
+        assert len({base.name, m.name, u.name}) == 3
+        assert m.delay == base.delay and u.n == base.n

@@ -13,7 +13,7 @@ import oracle
 from oracle.mlp import BF16, Shape
 from paper_2211_00889_amd import _lib, runner
 from synth import mlp_data, workloads
-from tests._util import mlp_blocks, pad_cols, rel_err_blocks
+from tests._util import mlp_blocks, pad_cols
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -61,7 +61,7 @@ def test_grad_small_shape_every_entry(tiny):
         for j in range(wl.m):
             if mask[i, j]:
                 g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
-                assert rel_err_blocks(G[i, j], g, mlp_blocks(*r.dims)) <= TOL_BF16, (i, j)
+                assert _grad_ok(G[i, j], X[i], A[idx[i, j]], y[idx[i, j]], s, r.dims), (i, j)
                 assert (G[i, j, s.n_params:] == 0).all()  # the padding
                 assert abs(L[i, j] - loss) <= TOL_BF16 * abs(loss)
             else:
@@ -108,7 +108,7 @@ def test_grad_and_loss_odd_shapes_every_entry(d_in, hidden, classes):
         for j in range(m):
             if mask[i, j]:
                 g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
-                assert rel_err_blocks(Gh[i, j], g, mlp_blocks(*dims)) <= TOL_BF16, (i, j)
+                assert _grad_ok(Gh[i, j], X[i], A[idx[i, j]], y[idx[i, j]], s, dims), (i, j)
                 assert (Gh[i, j, s.n_params:] == 0).all()
                 assert abs(Lh[i, j] - loss) <= TOL_BF16 * abs(loss)
             else:
@@ -120,9 +120,130 @@ def test_grad_and_loss_odd_shapes_every_entry(d_in, hidden, classes):
         assert abs(evh[k] - loss) <= TOL_BF16 * abs(loss), k
 
 
-def test_grad_full_shape_sampled_entries():
-    """The full shape in the runner's launch configuration: padded rows
-    (row_stride(P) = 2^21 floats apart) through nbsgd_mlp_grad_strided."""
+# Decisions taken from floating point.  Both sides multiply the same bf16
+# operands exactly; the matrix cores add the products in fp32 (the forward in
+# four d_in slices), the oracle in fp64, and the sums differ by about 1e-7 to
+# 1e-6 at these shapes.  Where a value lies that close to a boundary, the two
+# sides may decide differently:
+# * the ReLU of a first-layer pre-activation within AMBIGUOUS of zero;
+# * the bf16 rounding of H = relu(Z1) (within AMBIGUOUS of a rounding
+#   midpoint), of dZ2 and of dZ1 (within BF16_WINDOW, relative, of one).
+# The thresholds keep a twenty-fold margin over the measured differences.  A
+# different decision moves the gradient entries that the value feeds by one
+# sample's share (ReLU) or one bf16 step of it (rounding); those entries get
+# that amount as an allowance on top of the 1e-2 bar, every other entry is
+# held to the bar alone.
+AMBIGUOUS = 2e-5
+BF16_WINDOW = 1e-5
+
+
+def _bf16_near_midpoint(v, window_rel):
+    """(mask, bf16 step): entries of v whose fp32 value lies within
+    window_rel * |v| of a bf16 rounding midpoint, and the bf16 spacing at v."""
+    f = np.asarray(v, np.float64).astype(np.float32)
+    low = (f.view(np.uint32) & np.uint32(0xFFFF)).astype(np.float64)
+    fulp = np.spacing(np.abs(f)).astype(np.float64)  # fp32 spacing at v
+    near = np.abs(low - 32768.0) * fulp <= window_rel * np.abs(f.astype(np.float64))
+    step = fulp * 65536.0
+    return near & (f != 0), step
+
+
+def _flip_allowance(params, Ab, yb, s):
+    """(allowance per parameter, decisions): the gradient entries each
+    undetermined decision of the mini-batch feeds, with the amount a
+    different decision moves them, from the oracle's own intermediates."""
+    q = oracle.mlp.bf16_round
+    W1, b1, W2, b2 = oracle.mlp.unpack(params, s)
+    Aq, W1q, W2q = q(Ab), q(W1), q(W2)
+    Z1 = Aq @ W1q + b1
+    act = Z1 > 0.0
+    H = np.maximum(Z1, 0.0)
+    Hq = q(H)
+    Z2 = Hq @ W2q + b2
+    P = np.exp(Z2 - Z2.max(axis=1, keepdims=True))
+    P /= P.sum(axis=1, keepdims=True)
+    P[np.arange(len(yb)), yb] -= 1.0
+    dZ2 = P / len(yb)
+    dZ2q = q(dZ2)
+    dH = dZ2q @ W2q.T
+    dZ1 = dH * act
+    w1, o_b1, o_w2, o_b2 = s.offsets()
+    allow = np.zeros(s.n_params)
+    aW1 = allow[:o_b1].reshape(s.d_in, s.hidden)
+    aW2 = allow[o_w2:o_b2].reshape(s.hidden, s.classes)
+    ab1 = allow[o_b1:o_w2]
+    absA = np.abs(Aq)
+    count = 0
+    # ReLU decisions
+    for r, h in zip(*np.nonzero(np.abs(Z1) < AMBIGUOUS)):
+        aW1[:, h] += absA[r] * abs(dH[r, h])
+        ab1[h] += abs(dH[r, h])
+        aW2[h, :] += AMBIGUOUS * np.abs(dZ2q[r])
+        count += 1
+    # bf16 rounding of H (absolute window, the error of Z1)
+    nearH, stepH = _bf16_near_midpoint(H, AMBIGUOUS / np.maximum(H, 1e-30))
+    for r, h in zip(*np.nonzero(nearH)):
+        aW2[h, :] += stepH[r, h] * np.abs(dZ2q[r])
+        count += 1
+    # bf16 rounding of dZ2
+    # (dZ2 = softmax - onehot cancels for a confident class: its fp32 error is
+    # absolute, about 1e-9 after the 1/b scale, so the window has that floor)
+    nearZ, stepZ = _bf16_near_midpoint(dZ2, np.maximum(BF16_WINDOW, 2e-8 / np.maximum(np.abs(dZ2), 1e-30)))
+    for r, c in zip(*np.nonzero(nearZ)):
+        aW2[:, c] += stepZ[r, c] * Hq[r]
+        feed = stepZ[r, c] * np.abs(W2q[:, c]) * act[r]  # dH[r, :] moves by this
+        aW1 += np.outer(absA[r], feed)
+        ab1 += feed
+        count += 1
+    # bf16 rounding of dZ1
+    nearD, stepD = _bf16_near_midpoint(dZ1, BF16_WINDOW)
+    for r, h in zip(*np.nonzero(nearD)):
+        aW1[:, h] += absA[r] * stepD[r, h]
+        count += 1
+    allow *= 1.01
+    return allow, count
+
+
+def _allowance_is_the_exception(allow, want, blocks, hidden):
+    """Few of each block's entries get an allowance larger than the bar
+    itself: at most 1% of them, or two hidden units' worth (a ReLU decision
+    covers a unit's whole dW1 column)."""
+    for _, a, b in blocks:
+        w = want[..., a:b]
+        rms = float(np.sqrt(np.mean(w * w))) or 1.0
+        assert float(np.mean(allow[..., a:b] > TOL_BF16 * rms)) <= max(0.01, 2.0 / hidden)
+
+
+def _within(got, want, blocks, allow=None):
+    """Element-wise bar: |got - want| <= 1e-2 * max(|want|, rms of want's
+    block) + allowance, for every element of every block."""
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    worst = 0.0
+    for _, a, b in blocks:
+        w = want[..., a:b]
+        rms = float(np.sqrt(np.mean(w * w))) or 1.0
+        excess = np.abs(got[..., a:b] - w) - (0.0 if allow is None else allow[..., a:b])
+        worst = max(worst, float(np.max(excess / np.maximum(np.abs(w), rms))))
+    return worst <= TOL_BF16, worst
+
+
+def _grad_ok(got, params, Ab, yb, s, dims):
+    """One mini-batch gradient against the oracle's at the same parameters:
+    element-wise at 1e-2 per block, with the undetermined decisions'
+    allowances."""
+    g, _ = oracle.mlp.grad(params, Ab, yb, s, BF16)
+    allow, _ = _flip_allowance(params, Ab, yb, s)
+    _allowance_is_the_exception(allow, g, mlp_blocks(*dims), s.hidden)
+    ok, worst = _within(np.asarray(got)[:s.n_params], g, mlp_blocks(*dims), allow)
+    return ok
+
+
+def test_grad_full_shape_every_entry():
+    """The full shape in the runner's launch configuration (padded rows,
+    row_stride(P) = 2^21 floats apart, nbsgd_mlp_grad_strided): every
+    finished mini-batch's gradient, element by element, and its loss against
+    the oracle."""
     wl = workloads.MLP
     s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
     A, y, x0 = _data(wl)
@@ -136,10 +257,14 @@ def test_grad_full_shape_sampled_entries():
                           r.workspace)
     torch.cuda.synchronize()
     L = r.losses.cpu().numpy().reshape(wl.n, wl.m)
-    finished = list(zip(*np.nonzero(mask)))
-    for (i, j) in [finished[0], finished[len(finished) // 2], finished[-1]]:
+    G = r.G.cpu().numpy()
+    blocks = mlp_blocks(*r.dims)
+    for i, j in zip(*np.nonzero(mask)):
         g, loss = oracle.mlp.grad(x0, A[idx[i, j]], y[idx[i, j]], s, BF16)
-        assert rel_err_blocks(r.G[i, j].cpu().numpy(), g, mlp_blocks(*r.dims)) <= TOL_BF16
+        allow, _ = _flip_allowance(x0, A[idx[i, j]], y[idx[i, j]], s)
+        _allowance_is_the_exception(allow, g, blocks, wl.hidden)
+        ok, worst = _within(G[i, j, :s.n_params], g, blocks, allow)
+        assert ok, (i, j, worst)
         assert abs(L[i, j] - loss) <= TOL_BF16 * abs(loss)
     # every finished row: the layout padding inside P is zero, the row
     # padding beyond P untouched; unfinished rows untouched
@@ -150,7 +275,85 @@ def test_grad_full_shape_sampled_entries():
                 assert (tail[i, j, :r.P - s.n_params] == 0).all()
                 assert (tail[i, j, r.P - s.n_params:] == 7.0).all()
             else:
-                assert (tail[i, j] == 7.0).all() and (r.G[i, j, :64] == 7.0).all()
+                assert (tail[i, j] == 7.0).all() and (G[i, j, :64] == 7.0).all()
+
+
+def _iteration_from_common_state(wl, k, A, y, x0):
+    """One whole iteration of an MLP workload (gradients of every finished
+    mini-batch on the matrix cores, then the fused step) from a state both
+    sides share: the initial replicas (k = 0) or the oracle's own state after
+    k iterations, rounded to fp32 and given to both.  Every finished G row and
+    loss, and X and V, element by element against one oracle iteration, with
+    the allowances of the undetermined decisions (_flip_allowance) carried
+    through the step."""
+    s = Shape(wl.d_in, wl.hidden, wl.classes, wl.batch)
+    if k == 0:
+        X = np.tile(x0.astype(np.float64), (wl.n, 1))
+        V = np.zeros_like(X)
+    else:
+        ref = oracle.mlp.train(wl, A, y, x0, k, evaluate=False)
+        X, V = ref["X"], ref["V"]
+    X32, V32 = X.astype(np.float32), V.astype(np.float32)
+    r = runner.MlpRunner(wl, DEV, A, y, x0)
+    r.X[:, :s.n_params] = torch.from_numpy(X32).to(DEV)
+    r.V[:, :s.n_params] = torch.from_numpy(V32).to(DEV)
+    mask, counts, _ = r.step(k)
+    torch.cuda.synchronize()
+    G = r.G.cpu().numpy()
+    Xg, Vg = r.X.cpu().numpy(), r.V.cpu().numpy()
+    L = r.losses.cpu().numpy().reshape(wl.n, wl.m)
+
+    sch = oracle.schedule.sample_schedule(wl.seed, k, wl.n, wl.m, oracle.workload.delay(wl))
+    assert np.array_equal(sch["mask"], mask)
+    shuf = oracle.mlp.Shuffler(wl.seed, wl.shard, wl.m, wl.batch)
+    Xs, Vs = X32.astype(np.float64), V32.astype(np.float64)
+    Go = np.zeros((wl.n, wl.m, s.n_params))
+    allow_v = np.zeros((wl.n, s.n_params))
+    blocks = mlp_blocks(*r.dims)
+    for i in range(wl.n):
+        rows = shuf.indices(k, i)
+        for j in range(wl.m):
+            if not mask[i, j]:
+                continue
+            Go[i, j], loss = oracle.mlp.grad(Xs[i], A[rows[j]], y[rows[j]], s, BF16)
+            allow, _ = _flip_allowance(Xs[i], A[rows[j]], y[rows[j]], s)
+            _allowance_is_the_exception(allow, Go[i, j], blocks, wl.hidden)
+            ok, worst = _within(G[i, j, :s.n_params], Go[i, j], blocks, allow)
+            assert ok, ("G", i, j, worst)
+            assert abs(L[i, j] - loss) <= TOL_BF16 * abs(loss)
+            allow_v[i] += allow / counts[i]
+    W = oracle.workload.mixer(wl).w(k)
+    lr, mu = float(np.float32(wl.lr)), float(np.float32(wl.momentum))
+    order = oracle.workload.order(wl)
+    Xo, Vo = oracle.step.step(Xs, Vs, Go, mask, W, lr, mu, order)
+    ok, worst = _within(Vg[:, :s.n_params], Vo, blocks, allow_v)
+    assert ok, ("V", worst)
+    eta_allow = (lr * counts / wl.m)[:, None] * allow_v
+    if order == oracle.step.STEP_THEN_MIX:  # the stepped rows are mixed
+        eta_allow = np.abs(W) @ eta_allow
+    ok, worst = _within(Xg[:, :s.n_params], Xo, blocks, eta_allow)
+    assert ok, ("X", worst)
+    assert (Xg[:, s.n_params:] == 0).all() and (Vg[:, s.n_params:] == 0).all()
+
+
+@pytest.mark.parametrize("k", [0, 12])
+def test_full_shape_iteration_from_common_state(k):
+    """The full workload (D-PSGD ring), from its initial replicas and from the
+    oracle's state after 12 iterations."""
+    wl = workloads.MLP
+    _say(f"mlp full-shape iteration {k} from a common state")
+    _iteration_from_common_state(wl, k, *_data(wl))
+
+
+@pytest.mark.parametrize("kind", ["ring", "matcha", "uniform"])
+@pytest.mark.parametrize("k", [0, 7, 11])
+def test_small_shape_iteration_from_common_state(tiny, kind, k):
+    """Each mixing kind (D-PSGD ring, MATCHA, all-reduce with uniform W) on
+    the small workload, from the oracle's own states along its run."""
+    wl, A, y, x0 = tiny
+    wl = workloads.mlp_with_mixing(wl, kind)
+    _say(f"mlp {wl.name} iteration {k} from a common state")
+    _iteration_from_common_state(wl, k, A, y, x0)
 
 
 def test_grad_strided_rows_match_contiguous_small_shape(tiny):
@@ -182,12 +385,16 @@ def test_grad_strided_rows_match_contiguous_small_shape(tiny):
     assert (Gs[:, :, P:] == 7.0).all()
     Gn = Gc.cpu().numpy()
     for (i, j) in list(zip(*np.nonzero(mask)))[:3]:
-        g, _ = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
-        assert rel_err_blocks(Gn[i, j], g, mlp_blocks(*r.dims)) <= TOL_BF16, (i, j)
+        assert _grad_ok(Gn[i, j], X[i], A[idx[i, j]], y[idx[i, j]], s, r.dims), (i, j)
 
 
-def test_training_small_shape_matches_oracle(tiny):
+@pytest.mark.parametrize("kind", ["ring", "matcha", "uniform"])
+def test_training_small_shape_matches_oracle(tiny, kind):
+    """Non-blocking training under each mixing kind (D-PSGD ring, MATCHA,
+    all-reduce with uniform W) against the oracle's run of the same
+    workload."""
     wl, A, y, x0 = tiny
+    wl = workloads.mlp_with_mixing(wl, kind)
     _say(f"mlp training {wl.name} steps={wl.steps}")
     r = runner.MlpRunner(wl, DEV, A, y, x0)
     step_loss, counts = [], []
@@ -202,9 +409,19 @@ def test_training_small_shape_matches_oracle(tiny):
     assert np.array_equal(np.array(counts), np.array(ref["counts"]))
     np.testing.assert_allclose(step_loss, ref["step_loss"], rtol=TOL_BF16)
     assert abs(ev - ref["eval_loss"][-1]) <= TOL_BF16 * ref["eval_loss"][-1]
-    blocks = mlp_blocks(*r.dims)
-    assert rel_err_blocks(r.X.cpu().numpy(), ref["X"], blocks) <= TOL_BF16
-    assert rel_err_blocks(r.V.cpu().numpy(), ref["V"], blocks) <= TOL_BF16
+    # Over a trajectory the element-level parameters are not unique: a ReLU
+    # or bf16 rounding decision taken differently (see AMBIGUOUS) moves a
+    # unit's parameters, which moves that unit's pre-activations of later
+    # samples, and a unit whose pre-activations hover near zero amplifies
+    # that from step to step.  The element-wise bar is held one iteration at
+    # a time from common states (test_small_shape_iteration_from_common_state);
+    # here X and V are compared block by block by their rms gap, at 1e-2 of
+    # the parameters (X) and 5% of the momentum (V).
+    for name, a, b in mlp_blocks(*r.dims):
+        for got, want, bar in ((r.X.cpu().numpy()[:, a:b], ref["X"][:, a:b], TOL_BF16),
+                               (r.V.cpu().numpy()[:, a:b], ref["V"][:, a:b], 0.05)):
+            gap = np.sqrt(np.mean((got - want) ** 2))
+            assert gap <= bar * np.sqrt(np.mean(want ** 2)), (name, gap)
 
 
 def test_eval_loss_of_average_replica(tiny):
@@ -268,12 +485,15 @@ def test_full_workload_trajectory_matches_golden():
         assert gap <= 0.1 * moved, name
 
 
-def test_blocking_baseline_small_shape_matches_oracle(tiny):
-    """The D-PSGD baseline (every mini-batch finished, iteration time T_sync)
-    on the same kernels, against the oracle's blocking run."""
+@pytest.mark.parametrize("kind", ["ring", "matcha", "uniform"])
+def test_blocking_baseline_small_shape_matches_oracle(tiny, kind):
+    """The synchronous baselines (D-PSGD, MATCHA, all-reduce: every
+    mini-batch finished, iteration time T_sync) on the same kernels, against
+    the oracle's blocking run."""
     wl, A, y, x0 = tiny
-    wl = dataclasses.replace(wl, delay=workloads.DelaySpec("const", 1.0, 0.0, slow_learner=-2,
-                                                           slow_factor=2.0, slow_prob=0.5))
+    wl = dataclasses.replace(workloads.mlp_with_mixing(wl, kind),
+                             delay=workloads.DelaySpec("const", 1.0, 0.0, slow_learner=-2,
+                                                       slow_factor=2.0, slow_prob=0.5))
     _say(f"mlp blocking baseline {wl.name}")
     r = runner.MlpRunner(wl, DEV, A, y, x0)
     secs, step_loss = [], []
@@ -287,8 +507,11 @@ def test_blocking_baseline_small_shape_matches_oracle(tiny):
     ref = oracle.mlp.train(wl, A, y, x0, wl.steps, blocking=True)
     assert secs == ref["seconds"]  # bitwise: same fp64 schedule on both sides
     np.testing.assert_allclose(step_loss, ref["step_loss"], rtol=TOL_BF16)
-    blocks = mlp_blocks(*r.dims)
-    assert rel_err_blocks(r.X.cpu().numpy(), ref["X"], blocks) <= TOL_BF16
+    # parameters by their rms gap per block (the trajectory is not unique at
+    # the element level, see test_training_small_shape_matches_oracle)
+    for name, a, b in mlp_blocks(*r.dims):
+        got, want = r.X.cpu().numpy()[:, a:b], ref["X"][:, a:b]
+        assert np.sqrt(np.mean((got - want) ** 2)) <= TOL_BF16 * np.sqrt(np.mean(want ** 2)), name
     # the non-blocking schedule of the same iterations is never slower
     nb_secs = [runner.Schedule(wl).mask(k)[3][2] for k in range(wl.steps)]
     assert all(a <= b for a, b in zip(nb_secs, secs))
@@ -320,7 +543,7 @@ def test_grad_two_launch_groups_and_wide_indices():
     for k in picks:
         i, j = finished[k]
         g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
-        assert rel_err_blocks(r.G[i, j].cpu().numpy(), g, mlp_blocks(*r.dims)) <= TOL_BF16, (k, i, j)
+        assert _grad_ok(r.G[i, j].cpu().numpy(), X[i], A[idx[i, j]], y[idx[i, j]], s, r.dims), (k, i, j)
         assert abs(L[i, j] - loss) <= TOL_BF16 * abs(loss)
     assert (r.G[3, 10:] == 7.0).all() and (r.G[15, 1:] == 7.0).all()
 
@@ -367,7 +590,7 @@ def test_grad_indices_in_arguments_match_indices_through_workspace(finished, dim
     assert (Gp[~done] == 7.0).all() and (Lp[~done] == -1.0).all()
     for i, j in ((0, 0), (3, 5), (7, 7)):
         g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
-        assert rel_err_blocks(Gf[i, j], g, mlp_blocks(*dims)) <= TOL_BF16, (i, j)
+        assert _grad_ok(Gf[i, j], X[i], A[idx[i, j]], y[idx[i, j]], s, dims), (i, j)
         assert abs(Lf[i, j] - loss) <= TOL_BF16 * abs(loss)
 
 
@@ -390,7 +613,7 @@ def test_grad_largest_16_bit_sample_index():
     L = r.losses.cpu().numpy().reshape(wl.n, wl.m)
     for i, j in ((2, 3), (0, 0), (wl.n - 1, wl.m - 1)):
         g, loss = oracle.mlp.grad(X[i], A[idx[i, j]], y[idx[i, j]], s, BF16)
-        assert rel_err_blocks(r.G[i, j].cpu().numpy(), g, mlp_blocks(*r.dims)) <= TOL_BF16, (i, j)
+        assert _grad_ok(r.G[i, j].cpu().numpy(), X[i], A[idx[i, j]], y[idx[i, j]], s, r.dims), (i, j)
         assert abs(L[i, j] - loss) <= TOL_BF16 * abs(loss)
 
 
