@@ -30,6 +30,7 @@
 #include <vector>
 
 #include "internal.h"
+#include "mlp_shape.h"
 
 using namespace nbsgd;
 
@@ -38,20 +39,10 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBatch = 32;       // mini-batch size (the MFMA K of dW1)
-constexpr int kMaxHidden = 512;
-constexpr int kMaxClasses = 16;  // classes fill one 16-wide MFMA tile
+// kBatch, kMaxHidden, kMaxClasses, kFeatBlock, kSkMaxSlices and Dims: mlp_shape.h
 constexpr int kMaxList = 896;    // mini-batches per launch group (kernel-argument list)
 constexpr int kMaxEval = 512;    // batches of 32 per nbsgd_mlp_loss call
-constexpr int kFeatBlock = 128;  // d_in features per k_mlp_wgrad workgroup
 constexpr int kHeadThreads = 1024;  // 16 waves per mini-batch in k_mlp_head
-
-struct Dims {
-  int32_t d_in, hidden, classes;
-  int64_t P;                     // padded parameters per replica
-  int64_t ld;                    // floats from one row of X (and of G) to the next, >= P
-  int64_t off_b1, off_w2, off_b2, off_pad;
-};
 
 // One launch group's mini-batches, word e = learner << 24 | slot << 12,
 // sorted by learner.  A slot indexes the caller's sample list (slot * 32 ..),
@@ -121,7 +112,6 @@ __global__ void __launch_bounds__(256) k_put_idx(int32_t* __restrict__ dst, IdxC
 // the workgroups of slice 0 and unit block 0 copy them to the workspace for
 // the later kernels; otherwise they are read from the workspace.
 constexpr int kSkRows = 128, kSkUnits = 128, kSkKc = 64, kSkLd = kSkKc + 8;
-constexpr int kSkMaxSlices = 4;
 struct SkMap {
   int32_t n;              // learners present
   int32_t S;              // K slices
@@ -547,38 +537,6 @@ __global__ void __launch_bounds__(256)
 
 // ------------------------------------------------------------------ host
 
-nbsgd_status check_shape(const nbsgd_mlp_shape* s, Dims* d) {
-  if (!s) return fail(NBSGD_E_ARG, "shape is null");
-  if (s->batch != kBatch)
-    return fail(NBSGD_E_UNSUPPORTED, "batch=%d: only %d is supported", s->batch, kBatch);
-  if (s->d_in < kFeatBlock || s->d_in % kFeatBlock || s->hidden < 64 || s->hidden % 64 ||
-      s->hidden > kMaxHidden)
-    return fail(NBSGD_E_UNSUPPORTED,
-                "d_in=%d must be a multiple of %d and hidden=%d a multiple of 64, at most %d",
-                s->d_in, kFeatBlock, s->hidden, kMaxHidden);
-  if (s->classes < 2 || s->classes > kMaxClasses)
-    return fail(NBSGD_E_UNSUPPORTED, "classes=%d must be in [2, %d]", s->classes, kMaxClasses);
-  d->d_in = s->d_in;
-  d->hidden = s->hidden;
-  d->classes = s->classes;
-  d->off_b1 = (int64_t)s->d_in * s->hidden;
-  d->off_w2 = d->off_b1 + s->hidden;
-  d->off_b2 = d->off_w2 + (int64_t)s->hidden * s->classes;
-  d->off_pad = d->off_b2 + s->classes;
-  d->P = (d->off_pad + 3) & ~(int64_t)3;
-  d->ld = d->P;
-  return NBSGD_OK;
-}
-
-size_t up256(size_t b) { return (b + 255) & ~(size_t)255; }
-
-// sample list, dZ1 [rows/32][hidden][32] bf16 and kSkMaxSlices partial Z1
-// planes [rows][hidden] fp32, each 256-byte aligned
-size_t workspace_for(const Dims& d, int64_t rows) {
-  return up256((size_t)rows * 4) + up256((size_t)rows * d.hidden * 2) +
-         (size_t)kSkMaxSlices * up256((size_t)rows * d.hidden * 4);
-}
-
 struct Workspace {
   int32_t* idx;
   __bf16* dz1t;
@@ -706,25 +664,6 @@ void launch_group(const std::pair<int, int>* mb, int count, const int32_t* host_
 }
 
 }  // namespace
-
-extern "C" nbsgd_status nbsgd_mlp_param_count(const nbsgd_mlp_shape* s, int64_t* P) {
-  clear_error();
-  Dims d;
-  if (nbsgd_status st = check_shape(s, &d)) return st;
-  if (!P) return fail(NBSGD_E_ARG, "P is null");
-  *P = d.P;
-  return NBSGD_OK;
-}
-
-extern "C" nbsgd_status nbsgd_mlp_workspace_bytes(const nbsgd_mlp_shape* s, int64_t rows,
-                                                  size_t* bytes) {
-  clear_error();
-  Dims d;
-  if (nbsgd_status st = check_shape(s, &d)) return st;
-  if (!bytes || rows < 0) return fail(NBSGD_E_ARG, "bytes is null or rows < 0");
-  *bytes = workspace_for(d, rows);
-  return NBSGD_OK;
-}
 
 namespace {
 

@@ -39,6 +39,7 @@
 #include <algorithm>
 
 #include "internal.h"
+#include "plan.h"
 
 using namespace nbsgd;
 
@@ -47,15 +48,9 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kWaves = 4;
 constexpr int kBlock = kWave * kWaves;
-constexpr int kMaxN = NBSGD_MAX_LEARNERS;
-constexpr int kMaxM = NBSGD_MAX_MINIBATCHES;
-
-// fused step kernel shape
-constexpr int kStepWaves = 8;
+// fused step kernel shape (kStepWaves, kMaxRuns: plan.h)
 constexpr int kStepBlock = kWave * kStepWaves;
 constexpr int kStepSlots = (kMaxN + kStepWaves - 1) / kStepWaves;
-constexpr int kMaxRows = kMaxN * kMaxM;           // finished rows of one step
-constexpr int kMaxRuns = kMaxN + kStepWaves - 1;  // partial-sum slots
 // the fused step's LDS: n rows of values to mix and one row per run, 64 lanes
 // of float4 each; within the 64 KiB a workgroup may allocate
 static_assert((kMaxN + kMaxRuns) * kWave * 4 * sizeof(float) <= 64 * 1024,
@@ -82,57 +77,16 @@ struct Vec<1> {
 // form a scalar-load base address that was not 4-byte aligned; the scalar
 // memory unit ignores the low two address bits, so neighbouring fields were
 // read one element early.)
-__host__ __device__ __forceinline__ uint32_t byte_of(const uint32_t* words, int i) {
+__device__ __forceinline__ uint32_t byte_of(const uint32_t* words, int i) {
   return (words[i >> 2] >> (8 * (i & 3))) & 0xffu;
 }
-__host__ __device__ __forceinline__ uint32_t half_of(const uint32_t* words, int i) {
+__device__ __forceinline__ uint32_t half_of(const uint32_t* words, int i) {
   return (words[i >> 1] >> (16 * (i & 1))) & 0xffffu;
 }
-__host__ __device__ __forceinline__ void set_byte(uint32_t* words, int i, uint32_t v) {
-  words[i >> 2] |= (v & 0xffu) << (8 * (i & 3));
-}
-__host__ __device__ __forceinline__ void set_half(uint32_t* words, int i, uint32_t v) {
-  words[i >> 1] |= (v & 0xffffu) << (16 * (i & 1));
-}
-
-// Per-learner constants of one step, passed by value in the kernel arguments.
-struct Learners {
-  float eta[kMaxN];           // lr * c_i / m
-  float inv_c[kMaxN];         // 1 / c_i
-  int32_t count[kMaxN];       // c_i
-  // indices of the finished mini-batches, four 8-bit indices per word so the
-  // kernel reads them with scalar loads
-  uint32_t rows[kMaxN][kMaxM / 4];
-};
 
 __device__ __forceinline__ int row_of(const Learners& L, int p, int r) {
   return (int)byte_of(L.rows[p], r);
 }
-
-// Mixing matrix as CSR over its nonzero entries, or the uniform flag.
-struct Mixing {
-  int32_t uniform;   // all entries equal: out = (sum_p z_p) * w_all
-  float w_all;
-  int32_t start[kMaxN + 1];
-  uint32_t col[kMaxN * kMaxN / 4];  // column of each entry, 8 bits each
-  float w[kMaxN * kMaxN];
-};
-
-// Per-step plan of the fused kernel, passed by value in the kernel arguments.
-// Entries are the finished (learner, mini-batch) pairs in learner-major
-// order; wave w sums entries [seg[w], seg[w+1]).  A run is a maximal stretch
-// of one learner's entries inside one wave's segment; runs are numbered in
-// entry order and each owns one LDS slot.
-struct StepPlan {
-  float eta[kMaxN];                    // lr * c_i / m
-  float inv_c[kMaxN];                  // 1 / c_i
-  int32_t prefix[kMaxN + 2];           // first entry of each learner; [n] = [n+1] = total
-  int32_t seg[kStepWaves + 1];         // first entry of each wave's segment
-  int32_t seg_p[kStepWaves];           // learner of a segment's first entry
-  int32_t seg_slot[kStepWaves];        // slot of a segment's first run
-  int32_t lslot[kMaxN + 1];            // slots of learner p: [lslot[p], lslot[p+1])
-  uint32_t row[(kMaxRows + 16) / 2];   // G row (p * m + j) of each entry, 16 bits each
-};
 
 template <typename T>
 __device__ __forceinline__ T ld_stream(const T* p) {
@@ -356,45 +310,6 @@ bool overlap(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
   return a0 < b0 + (uintptr_t)b_bytes && b0 < a0 + (uintptr_t)a_bytes;
 }
 
-nbsgd_status learners_from_mask(const uint8_t* mask, int32_t n, int32_t m, float lr, Learners* L) {
-  if (!mask) return fail(NBSGD_E_ARG, "mask is null");
-  memset(L, 0, sizeof *L);
-  for (int32_t i = 0; i < n; ++i) {
-    int32_t c = 0;
-    for (int32_t j = 0; j < m; ++j)
-      if (mask[i * m + j]) {
-        L->rows[i][c >> 2] |= (uint32_t)j << (8 * (c & 3));
-        ++c;
-      }
-    if (c == 0) return fail(NBSGD_E_MASK, "learner %d finished no mini-batch", i);
-    L->count[i] = c;
-    L->inv_c[i] = (float)(1.0 / (double)c);
-    L->eta[i] = (float)((double)lr * (double)c / (double)m);
-  }
-  return NBSGD_OK;
-}
-
-nbsgd_status mixing_from_w(const float* Wh, int32_t n, Mixing* W) {
-  if (nbsgd_status st = check_w(Wh, n)) return st;
-  memset(W, 0, sizeof *W);
-  W->uniform = 1;
-  for (int32_t k = 1; k < n * n; ++k)
-    if (Wh[k] != Wh[0]) W->uniform = 0;
-  W->w_all = Wh[0];
-  int32_t e = 0;
-  for (int32_t i = 0; i < n; ++i) {
-    W->start[i] = e;
-    for (int32_t p = 0; p < n; ++p)
-      if (Wh[i * n + p] != 0.0f) {
-        set_byte(W->col, e, (uint32_t)p);
-        W->w[e] = Wh[i * n + p];
-        ++e;
-      }
-  }
-  W->start[n] = e;
-  return NBSGD_OK;
-}
-
 nbsgd_status check_launch(const char* what) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(NBSGD_E_HIP, "%s launch failed: %s", what, hipGetErrorString(e));
@@ -409,43 +324,6 @@ nbsgd_status check_rows(const void* p, const char* name) {
 
 static_assert(sizeof(StepPlan) + sizeof(Mixing) + 64 <= 4096, "kernel arguments exceed 4 KiB");
 
-nbsgd_status plan_from_mask(const uint8_t* mask, int32_t n, int32_t m, float lr, StepPlan* S,
-                            int* runs) {
-  if (!mask) return fail(NBSGD_E_ARG, "mask is null");
-  memset(S, 0, sizeof *S);
-  int32_t e = 0;
-  int learner_of[kMaxRows];
-  for (int32_t i = 0; i < n; ++i) {
-    S->prefix[i] = e;
-    for (int32_t j = 0; j < m; ++j)
-      if (mask[i * m + j]) {
-        learner_of[e] = i;
-        set_half(S->row, e++, (uint32_t)(i * m + j));
-      }
-    const int32_t c = e - S->prefix[i];
-    if (c == 0) return fail(NBSGD_E_MASK, "learner %d finished no mini-batch", i);
-    S->inv_c[i] = (float)(1.0 / (double)c);
-    S->eta[i] = (float)((double)lr * (double)c / (double)m);
-  }
-  S->prefix[n] = S->prefix[n + 1] = e;
-  int slot = 0, last_learner = -1;
-  for (int w = 0; w <= kStepWaves; ++w) S->seg[w] = (int32_t)((int64_t)w * e / kStepWaves);
-  for (int w = 0; w < kStepWaves; ++w) {
-    S->seg_slot[w] = slot;
-    if (S->seg[w] == S->seg[w + 1]) continue;
-    S->seg_p[w] = learner_of[S->seg[w]];
-    for (int32_t k = S->seg[w]; k < S->seg[w + 1]; ++k) {
-      const bool starts_run = k == S->seg[w] || learner_of[k] != learner_of[k - 1];
-      if (!starts_run) continue;
-      while (last_learner < learner_of[k]) S->lslot[++last_learner] = slot;
-      ++slot;
-    }
-  }
-  while (last_learner < n) S->lslot[++last_learner] = slot;
-  *runs = slot;
-  return NBSGD_OK;
-}
-
 template <int VEC, int ORDER>
 void launch_step(float* X, float* V, const float* G, int64_t pv, int64_t ldv, int n, float mu,
                  const StepPlan& S, int runs, const Mixing& W, hipStream_t s) {
@@ -454,11 +332,6 @@ void launch_step(float* X, float* V, const float* G, int64_t pv, int64_t ldv, in
   hipLaunchKernelGGL((k_step<VEC, ORDER>), dim3((unsigned)blocks), dim3(kStepBlock), lds, s, X,
                      V, G, pv, ldv, n, mu, S, W);
 }
-
-// Row strides of nbsgd_row_stride: rows longer than 2^22 floats (16 MiB)
-// start on 16 MiB boundaries; rows of 2^20 floats or fewer are not padded.
-constexpr int64_t kRowAlign = int64_t(1) << 22;
-constexpr int64_t kSmallRow = int64_t(1) << 20;
 
 // The fused step on rows `ld` floats apart (ld >= P).
 nbsgd_status step_impl(float* X, float* V, const float* G, int64_t ld, const uint8_t* mask,
@@ -515,26 +388,6 @@ extern "C" nbsgd_status nbsgd_step_strided(float* X, float* V, const float* G, i
                                            int32_t order, void* stream) {
   clear_error();
   return step_impl(X, V, G, ld, mask, Wh, n, m, P, lr, momentum, order, stream);
-}
-
-extern "C" nbsgd_status nbsgd_row_stride(int64_t P, int64_t* ld) {
-  clear_error();
-  if (!ld) return fail(NBSGD_E_ARG, "ld is null");
-  if (P < 0) return fail(NBSGD_E_SHAPE, "P=%lld is negative", (long long)P);
-  if (P <= kSmallRow) {
-    *ld = P;
-    return NBSGD_OK;
-  }
-  if (P <= kRowAlign) {  // the next power of two, 2^21 or 2^22
-    int64_t p2 = kSmallRow;
-    while (p2 < P) p2 <<= 1;
-    *ld = p2;
-    return NBSGD_OK;
-  }
-  int64_t k = (P + kRowAlign - 1) / kRowAlign;  // rows of k * 2^22 floats, k >= 2
-  if ((k & (k - 1)) == 0) ++k;  // a power-of-two stride aliases
-  *ld = k * kRowAlign;
-  return NBSGD_OK;
 }
 
 extern "C" nbsgd_status nbsgd_accumulate(const float* G, const uint8_t* mask, int32_t n, int32_t m,
