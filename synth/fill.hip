@@ -3,7 +3,10 @@
 // or 24-bit uniform shaping, one correctly rounded fp32 multiply).  Holds no
 // arithmetic of the optimisation method itself.
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
+
+#include "synth.h"
 
 namespace {
 
@@ -38,6 +41,15 @@ __global__ void __launch_bounds__(256) fill_kernel(float* __restrict__ dst, int6
   }
 }
 
+uint64_t fmix_host(uint64_t z) {
+  z ^= z >> 30;
+  z *= 0xBF58476D1CE4E5B9ull;
+  z ^= z >> 27;
+  z *= 0x94D049BB133111EBull;
+  z ^= z >> 31;
+  return z;
+}
+
 }  // namespace
 
 extern "C" {
@@ -59,6 +71,14 @@ int synth_fill(float* dst, int64_t count, int64_t first, uint64_t key, float sca
     hipLaunchKernelGGL(fill_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, s, dst, count, first,
                        key, scale);
   return (int)hipGetLastError();
+}
+
+int synth_fill_normal(float* dst, int64_t count, int64_t first, uint64_t seed, uint64_t stream_id,
+                      double std, void* stream) {
+  const uint64_t key = fmix_host(fmix_host(seed + kGamma) + (stream_id + 1) * kGamma);
+  // standard deviation of the centred sum of four uniform 16-bit integers
+  const double unit = sqrt((65536.0 * 65536.0 - 1.0) / 3.0);
+  return synth_fill(dst, count, first, key, (float)(std / unit), 0, stream);
 }
 
 }  // extern "C"
