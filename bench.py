@@ -337,16 +337,26 @@ def bench_unfused(args):
 
 def time_step_workload(wl, args, dev):
     """Times K back-to-back fused steps of a step workload after W warm-up
-    steps, on resident buffers; returns the figures of one bench record."""
+    steps, on resident buffers; returns the figures of one bench record.
+    With ``args.server`` the step is Alg. 3's parameter-server form
+    (nbsgd_step_server) on row 0 of X as the server model, V and G."""
     import torch
 
-    from paper_2211_00889_amd import runner
+    from paper_2211_00889_amd import _lib, runner
 
     r = runner.StepRunner(wl, dev)
     stream = torch.cuda.current_stream(dev)
+    server = getattr(args, "server", False)
+
+    def launch(mask, W):
+        if server:
+            _lib.step_server(r.Xrows[0], r.Vrows, r.Grows, wl.P, mask, wl.lr, wl.momentum)
+        else:
+            r.launch(mask, W)
+
     for k in range(args.warmup):
         mask, counts, _, W = r.plan(k)
-        r.launch(mask, W)
+        launch(mask, W)
     torch.cuda.synchronize()
 
     # Two events bracket the K launches on their stream: the launches run back
@@ -363,7 +373,7 @@ def time_step_workload(wl, args, dev):
         t_plan = time.perf_counter()
         mask, counts, _, W = r.plan(args.warmup + i)
         plan_s.append(time.perf_counter() - t_plan)
-        r.launch(mask, W)
+        launch(mask, W)
         sum_counts.append(int(counts.sum()))
     end.record(stream)
     torch.cuda.synchronize()
@@ -373,7 +383,10 @@ def time_step_workload(wl, args, dev):
     torch.cuda.empty_cache()
 
     kern_ms_mean = start.elapsed_time(end) / K
-    alg_bytes = np.array([wl.alg_bytes(c) for c in sum_counts], dtype=np.float64)
+    if server:  # finished G rows, V read and written, the one server row read and written
+        alg_bytes = np.array([4 * wl.P * (c + 2 * wl.n + 2) for c in sum_counts], dtype=np.float64)
+    else:
+        alg_bytes = np.array([wl.alg_bytes(c) for c in sum_counts], dtype=np.float64)
     achieved = alg_bytes.sum() / (kern_ms_mean * K * 1e-3) / 1e9
     rec = {
         "value": wl.n * wl.P * K / wall,
@@ -389,7 +402,10 @@ def time_step_workload(wl, args, dev):
                      "kernel_ms_of": "HIP events around the K back-to-back launches, divided by K",
                      "alg_bytes_per_launch_mean": float(alg_bytes.mean())},
     }
-    tr = measured_traffic(wl)
+    if server:
+        rec["config"]["form"] = "parameter server (nbsgd_step_server, Alg. 3)"
+        rec["roofline"]["kernel"] = "k_step<server>"
+    tr = None if server else measured_traffic(wl)
     if tr is not None:
         rec["roofline"]["traffic"] = tr["traffic_bytes_per_launch"]
         rec["roofline"]["traffic_over_alg"] = tr["traffic_over_alg"]
@@ -418,6 +434,9 @@ def main():
                          "(launch-bound workloads such as --workload tiny)")
     ap.add_argument("--replays", type=int, default=200,
                     help="graph replays timed with --graph")
+    ap.add_argument("--server", action="store_true",
+                    help="time Alg. 3's parameter-server form of the step (nbsgd_step_server) "
+                         "on the workload's shape instead of the replica step")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="after the timed steps, run one plain 1 GiB device copy (torch's copy "
                          "kernel) so hardware byte counters can be scaled against known bytes")
@@ -499,7 +518,7 @@ def main():
               f"{rec['roofline']['frac']:.3f} of peak", file=sys.stderr, flush=True)
         rf = rec["roofline"]
         others.append({"workload": w.name, "value": rec["value"], "unit": UNIT,
-                       "ms_per_step": rec["ms_per_step"], "kernel": "k_step",
+                       "ms_per_step": rec["ms_per_step"], "kernel": rf["kernel"],
                        "kernel_ms_mean": rf["kernel_ms_mean"],
                        "alg_bytes_per_launch_mean": rf["alg_bytes_per_launch_mean"],
                        "achieved_GBs": rf["achieved"], "frac": rf["frac"],

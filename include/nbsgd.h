@@ -212,6 +212,24 @@ nbsgd_status nbsgd_step_strided(float *X, float *V, const float *G, int64_t ld,
                                 const uint8_t *mask, const float *W, int32_t n, int32_t m,
                                 int64_t P, float lr, float momentum, int32_t order, void *stream);
 
+/* Non-blocking synchronous centralized SGD (Alg. 3; the 1/n of Eq. 2
+ * restored): one server model x, each learner's momentum buffer and
+ * accumulated gradient (its finished mini-batches, evaluated at the server
+ * model by the caller), in one pass:
+ *   g_i = (1/c_i) sum_{finished j} G[i][j]      eta_i = lr * c_i / m
+ *   V[i] = momentum * V[i] + g_i
+ *   x    = x - (1/n) sum_i eta_i V[i]   (1/n in fp32, summed in learner order)
+ * x     device fp32 [P] (the server model), updated in place
+ * V, G  device fp32 rows `ld` floats apart as in nbsgd_step_strided:
+ *       V [n][ld] updated in place, G [n][m][ld] read (finished rows only)
+ * mask  host uint8 [n*m] as in nbsgd_step.  x, V and G must not overlap.
+ * HBM traffic: 4 * P * (sum_i c_i + 2n + 2) bytes, against 4 * P *
+ * (sum_i c_i + 4n) for the same update on n replicas of x with nbsgd_step.
+ * Errors: as nbsgd_step_strided.                                            */
+nbsgd_status nbsgd_step_server(float *x, float *V, const float *G, int64_t ld, const uint8_t *mask,
+                               int32_t n, int32_t m, int64_t P, float lr, float momentum,
+                               void *stream);
+
 /* Row stride (in floats) to allocate X, V and G with for nbsgd_step_strided:
  *   P <= 2^20:          P (no padding);
  *   2^20 < P <= 2^22:   the next power of two, 2^21 or 2^22;

@@ -26,6 +26,7 @@ from ._lib import (  # noqa: F401
     row_stride,
     sample_mask,
     step,
+    step_server,
     step_strided,
     update,
     w_allreduce,

@@ -24,7 +24,7 @@ MAX_LEARNERS, MAX_MINIBATCHES = 16, 64
 SLOW_NONE, SLOW_RANDOM = -1, -2
 
 EXPORTS = ("nbsgd_sample_mask", "nbsgd_iteration_accounting", "nbsgd_accumulate", "nbsgd_mix", "nbsgd_update", "nbsgd_step",
-           "nbsgd_step_strided", "nbsgd_row_stride",
+           "nbsgd_step_strided", "nbsgd_step_server", "nbsgd_row_stride",
            "nbsgd_w_allreduce", "nbsgd_w_ring", "nbsgd_matcha_create", "nbsgd_matcha_w",
            "nbsgd_matcha_matchings", "nbsgd_matcha_set", "nbsgd_matcha_get", "nbsgd_matcha_optimize",
            "nbsgd_matcha_destroy", "nbsgd_mlp_param_count",
@@ -79,6 +79,8 @@ def load():
                        _f32, _f32, _i32, _c_void_p],
         "nbsgd_step_strided": [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p, _i32, _i32,
                                _i64, _f32, _f32, _i32, _c_void_p],
+        "nbsgd_step_server": [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _i32, _i32, _i64, _f32,
+                              _f32, _c_void_p],
         "nbsgd_row_stride": [_i64, ctypes.POINTER(_i64)],
         "nbsgd_w_allreduce": [_i32, _c_void_p],
         "nbsgd_w_ring": [_i32, _c_void_p],
@@ -295,6 +297,17 @@ def step_strided(X, V, G, P: int, mask, W, lr: float, momentum: float, order: in
     W = _w32(W, n)
     _check(load().nbsgd_step_strided(_dev(X, "X"), _dev(V, "V"), _dev(G, "G"), ld, _host_ptr(mask),
                                      _host_ptr(W), n, m, P, lr, momentum, order, _stream(X, stream)))
+
+
+def step_server(x, V, G, P: int, mask, lr: float, momentum: float, stream=None):
+    """nbsgd_step_server: x [ld] or [P] (the server model), V [n, ld],
+    G [n, m, ld]; the first P columns of each row are the parameters."""
+    n, m, ld = G.shape
+    if tuple(V.shape) != (n, ld) or x.dim() != 1 or x.shape[0] < P:
+        raise ValueError("V must be [n, ld] and x hold P floats, with G [n, m, ld]")
+    mask = _u8(mask, (n, m))
+    _check(load().nbsgd_step_server(_dev(x, "x"), _dev(V, "V"), _dev(G, "G"), ld, _host_ptr(mask), n, m,
+                                    P, lr, momentum, _stream(x, stream)))
 
 
 def row_stride(P: int) -> int:

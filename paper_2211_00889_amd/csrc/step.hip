@@ -146,6 +146,10 @@ __device__ __forceinline__ typename Vec<VEC>::type mix_all(const typename Vec<VE
   return acc;
 }
 
+// The parameter-server form of the step (Alg. 3): X is the one server row,
+// and the new server model is x - (1/n) sum_p eta_p v_p.
+constexpr int kServer = 2;
+
 template <int VEC, int ORDER>
 __global__ void __launch_bounds__(kStepBlock)
     k_step(float* __restrict__ Xf, float* __restrict__ Vf, const float* __restrict__ Gf,
@@ -174,7 +178,7 @@ __global__ void __launch_bounds__(kStepBlock)
     xo[s] = (vf)(0.0f);
     vo[s] = (vf)(0.0f);
     if (p < n && live) {
-      xo[s] = ld_stream(X + (int64_t)p * ldv + v);
+      if (ORDER != kServer || p == 0) xo[s] = ld_stream(X + (int64_t)p * ldv + v);
       vo[s] = ld_stream(V + (int64_t)p * ldv + v);
     }
   }
@@ -223,14 +227,20 @@ __global__ void __launch_bounds__(kStepBlock)
       if (ORDER == NBSGD_MIX_THEN_STEP) {
         zs[q * kWave + lane] = xo[s];
         keep[s] = S.eta[q] * vn;
-      } else {
+      } else if (ORDER == NBSGD_STEP_THEN_MIX) {
         zs[q * kWave + lane] = xo[s] - S.eta[q] * vn;
+      } else {  // kServer: the learner's contribution eta_q v_q
+        zs[q * kWave + lane] = S.eta[q] * vn;
       }
     }
   }
   __syncthreads();
 
-  // phase 3: mix and write the new replicas
+  // phase 3: mix and write the new replicas (the server row: wave 0 only)
+  if (ORDER == kServer) {
+    if (wave == 0 && live) st_stream(X + v, xo[0] - mix_all<VEC>(zs, kWave, n, lane) * W.w_all);
+    return;
+  }
   vf total = (vf)(0.0f);
   if (W.uniform) total = mix_all<VEC>(zs, kWave, n, lane) * W.w_all;
 #pragma unroll
@@ -388,6 +398,39 @@ extern "C" nbsgd_status nbsgd_step_strided(float* X, float* V, const float* G, i
                                            int32_t order, void* stream) {
   clear_error();
   return step_impl(X, V, G, ld, mask, Wh, n, m, P, lr, momentum, order, stream);
+}
+
+extern "C" nbsgd_status nbsgd_step_server(float* x, float* V, const float* G, int64_t ld,
+                                          const uint8_t* mask, int32_t n, int32_t m, int64_t P,
+                                          float lr, float momentum, void* stream) {
+  clear_error();
+  if (nbsgd_status st = check_nm(n, m)) return st;
+  if (P < 0) return fail(NBSGD_E_SHAPE, "P=%lld is negative", (long long)P);
+  if (ld < P) return fail(NBSGD_E_SHAPE, "row stride %lld is below P=%lld", (long long)ld, (long long)P);
+  StepPlan S;
+  int runs = 0;
+  if (nbsgd_status st = plan_from_mask(mask, n, m, lr, &S, &runs)) return st;
+  Mixing W;  // the average over the n learners: 1/n, rounded once
+  memset(&W, 0, sizeof W);
+  W.uniform = 1;
+  W.w_all = (float)(1.0 / (double)n);
+  if (P == 0) return NBSGD_OK;
+  if (nbsgd_status st = check_rows(x, "x")) return st;
+  if (nbsgd_status st = check_rows(V, "V")) return st;
+  if (nbsgd_status st = check_rows(G, "G")) return st;
+  const int64_t vb = ((int64_t)(n - 1) * ld + P) * 4, gb = ((int64_t)n * m - 1) * ld * 4 + P * 4;
+  if (overlap(x, P * 4, V, vb)) return fail(NBSGD_E_ARG, "x and V overlap");
+  if (overlap(G, gb, x, P * 4) || overlap(G, gb, V, vb)) return fail(NBSGD_E_ARG, "G overlaps x or V");
+  const int vec = std::min(vec_width(P), vec_width(ld));
+  const int64_t pv = P / vec, ldv = ld / vec;
+  if ((pv + kWave - 1) / kWave > 0x7fffffff)
+    return fail(NBSGD_E_UNSUPPORTED, "P=%lld needs too many workgroups", (long long)P);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  // x is a single row: the kernel reads and writes row 0 only
+  if (vec == 4) launch_step<4, kServer>(x, V, G, pv, ldv, n, momentum, S, runs, W, s);
+  else if (vec == 2) launch_step<2, kServer>(x, V, G, pv, ldv, n, momentum, S, runs, W, s);
+  else launch_step<1, kServer>(x, V, G, pv, ldv, n, momentum, S, runs, W, s);
+  return check_launch("nbsgd_step_server");
 }
 
 extern "C" nbsgd_status nbsgd_accumulate(const float* G, const uint8_t* mask, int32_t n, int32_t m,

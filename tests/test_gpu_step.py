@@ -389,3 +389,57 @@ def test_parameter_server_variant():
     assert all(np.array_equal(out[0], out[i]) for i in range(n))
     assert rel_err(out[0], xo) <= TOL
     assert rel_err(Vd.cpu().numpy(), Vo) <= TOL
+
+
+@pytest.mark.parametrize("n,m,P,ld", [(6, 5, 40003, 40003), (8, 8, 20002, 20008), (16, 4, 16396, 16400),
+                                      (1, 3, 1030, 1036), (3, 64, 257, 260)])
+def test_step_server_matches_alg3(n, m, P, ld):
+    """nbsgd_step_server (Alg. 3 with the 1/n of Eq. 2) against the oracle's
+    parameter-server step over four iterations: non-prefix masks, rows ld
+    floats apart whose padding must stay untouched, float4/float2/float
+    streams (P % 4 = 3, 2, 0), one learner to 16."""
+    rng = np.random.default_rng(n * 1000 + P)
+    x = rng.standard_normal(P).astype(np.float32)
+    G = (0.03 * rng.standard_normal((n, m, P))).astype(np.float32)
+    xd = torch.full((ld,), 7.0, dtype=torch.float32, device=DEV)
+    xd[:P] = torch.from_numpy(x).to(DEV)
+    Vd = torch.full((n, ld), 7.0, dtype=torch.float32, device=DEV)
+    Vd[:, :P] = 0.0
+    Gd = torch.full((n, m, ld), 7.0, dtype=torch.float32, device=DEV)
+    Gd[:, :, :P] = torch.from_numpy(G).to(DEV)
+    xo, Vo = x.astype(np.float64), np.zeros((n, P))
+    lr, mu = 0.2, 0.9
+    for k in range(4):
+        mask = _random_mask(rng, n, m, prefix=(k % 2 == 0))
+        _say(f"parameter-server step n={n} m={m} P={P} ld={ld} iteration {k}")
+        nb.step_server(xd, Vd, Gd, P, mask, lr, mu)
+        xo, Vo = oracle.step.parameter_server_step(xo, Vo, G, mask, float(np.float32(lr)),
+                                                   float(np.float32(mu)))
+    torch.cuda.synchronize()
+    assert rel_err(xd[:P].cpu().numpy(), xo) <= TOL
+    assert rel_err(Vd[:, :P].cpu().numpy(), Vo) <= TOL
+    assert (xd[P:] == 7.0).all() and (Vd[:, P:] == 7.0).all()
+    assert (Gd[:, :, :P].cpu().numpy() == G).all() and (Gd[:, :, P:] == 7.0).all()
+
+
+def test_step_server_equals_step_then_mix_on_identical_replicas():
+    """The server form and the replica form of Alg. 3 (uniform W,
+    step-then-mix on n copies of the server model) give the same model up to
+    fp32 rounding, and the same momentum buffers bit for bit."""
+    n, m, P = 8, 6, 30000
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(P).astype(np.float32)
+    G = (0.03 * rng.standard_normal((n, m, P))).astype(np.float32)
+    xs = _dev(x.copy())
+    Vs = torch.zeros(n, P, dtype=torch.float32, device=DEV)
+    Xr = _dev(np.tile(x, (n, 1)))
+    Vr = torch.zeros(n, P, dtype=torch.float32, device=DEV)
+    Gd = _dev(G)
+    for k in range(3):
+        mask = _random_mask(rng, n, m)
+        _say(f"server vs replicas iteration {k}")
+        nb.step_server(xs, Vs, Gd, P, mask, 0.1, 0.9)
+        nb.step(Xr, Vr, Gd, mask, nb.w_allreduce(n), 0.1, 0.9, nb.STEP_THEN_MIX)
+    torch.cuda.synchronize()
+    assert torch.equal(Vs, Vr)
+    assert rel_err(xs.cpu().numpy(), Xr[0].cpu().numpy().astype(np.float64)) <= TOL

@@ -370,3 +370,27 @@ def test_iteration_accounting_errors():
                                           ctypes.byref(a)) == _lib.E_SHAPE
     assert lib.nbsgd_iteration_accounting(t.ctypes.data_as(ctypes.c_void_p), 17, 3,
                                           ctypes.byref(a)) == _lib.E_UNSUPPORTED
+
+
+def test_step_server_argument_errors_launch_nothing():
+    # fake device pointers: every check happens on the host before a launch
+    lib = _lib.load()
+    n, m, P, ld = 4, 3, 1000, 1024
+    mask = np.ones(n * m, np.uint8)
+    mp = mask.ctypes.data_as(ctypes.c_void_p)
+    x, V, G = 0x100000, 0x200000, 0x400000
+
+    def call(x=x, V=V, G=G, ld=ld, P=P, n=n, mask=mp):
+        return lib.nbsgd_step_server(ctypes.c_void_p(x), ctypes.c_void_p(V), ctypes.c_void_p(G), ld, mask,
+                                     n, m, P, 0.1, 0.9, None)
+
+    assert call(x=x + 4) == _lib.E_ALIGN
+    assert call(ld=P - 4) == _lib.E_SHAPE
+    assert call(V=x + 16) == _lib.E_ARG and b"overlap" in lib.nbsgd_last_error()
+    assert call(G=V + 64) == _lib.E_ARG
+    assert call(n=0) == _lib.E_SHAPE
+    assert call(n=17) == _lib.E_UNSUPPORTED
+    bad = np.ones(n * m, np.uint8)
+    bad[3:6] = 0  # learner 1 finished nothing
+    assert call(mask=bad.ctypes.data_as(ctypes.c_void_p)) == _lib.E_MASK
+    assert call(P=0) == _lib.OK  # an empty call
