@@ -102,8 +102,11 @@ __global__ void __launch_bounds__(256) k_put_idx(int32_t* __restrict__ dst, IdxC
 // Forward, split over d_in.  Work item: a quad (up to four mini-batches of one
 // learner, 128 rows), a block of 128 hidden units and one of S equal slices of
 // d_in (S = the largest divisor of d_in / 64 up to kSkMaxSlices).  Both operands
-// are staged through LDS in bf16 ([row][k] and [unit][k], padded rows), so a
-// 16-byte read is one MFMA fragment.  Eight waves: wave w takes rows
+// are staged through LDS in bf16 ([row][k] and [unit][k]), so a 16-byte read
+// is one MFMA fragment; the 16-byte k-octets of a row are XOR-swizzled so
+// that the fragment reads and the staging writes are free of bank conflicts
+// (A: 64 bf16 per row, octet o at o ^ (row % 8); W1: 80 bf16 per row, octet o
+// at o ^ (unit / 4 % 8); both measured at one LDS cycle per 256 bytes).  Eight waves: wave w takes rows
 // 32 (w % 4) .. +31 and units 64 (w / 4) .. +63 (2 x 4 accumulators).  The
 // partial sums go to slice s of the partial buffer; k_mlp_head adds the
 // slices in slice order.  The work items are split into eight equal ranges,
@@ -111,7 +114,7 @@ __global__ void __launch_bounds__(256) k_put_idx(int32_t* __restrict__ dst, IdxC
 // share an L2.  INLINE: the sample indices come from the kernel arguments and
 // the workgroups of slice 0 and unit block 0 copy them to the workspace for
 // the later kernels; otherwise they are read from the workspace.
-constexpr int kSkRows = 128, kSkUnits = 128, kSkKc = 64, kSkLd = kSkKc + 8;
+constexpr int kSkRows = 128, kSkUnits = 128, kSkKc = 64, kSkLdA = kSkKc, kSkLdW = kSkKc + 16;
 struct SkMap {
   int32_t n;              // learners present
   int32_t S;              // K slices
@@ -130,8 +133,8 @@ __global__ void __launch_bounds__(512)
                  int32_t* __restrict__ idx, float* __restrict__ Zpart, int64_t part_stride, Dims d,
                  SkMap M, Idx16<INLINE ? kInline * kBatch / 2 : 1> I) {
   constexpr int kDepth = 2;  // chunks loaded ahead of the one being staged
-  __shared__ __attribute__((aligned(16))) __bf16 As[2][kSkRows * kSkLd];
-  __shared__ __attribute__((aligned(16))) __bf16 Ws[2][kSkUnits * kSkLd];
+  __shared__ __attribute__((aligned(16))) __bf16 As[2][kSkRows * kSkLdA];
+  __shared__ __attribute__((aligned(16))) __bf16 Ws[2][kSkUnits * kSkLdW];
   const int xcd = blockIdx.x & 7;
   const int64_t total = M.off[M.n];
   const int g = (int)(xcd * total / 8) + (int)(blockIdx.x >> 3);
@@ -158,10 +161,18 @@ __global__ void __launch_bounds__(512)
   const int wr = wave & 3, wu = wave >> 2;
   const bool mma = 32 * wr < rows && 64 * wu < units;  // wave-uniform
 
-  // A staging: row tid / 4, k = 4 q + 16 j (+0..3), q = tid % 4
-  const int arow = tid >> 2, aq = tid & 3;
+  // A staging: wave w takes rows 16 w .. +15, four consecutive lanes per row
+  // (64 contiguous bytes, k = 4 q + 16 j + 0..3); the four rows of a 16-lane
+  // group are two apart, which with the swizzle spreads its writes over all
+  // banks.
+  const int aquad = lane >> 2, aq = lane & 3;
+  const int arow = 16 * wave + ((aquad >> 2) & 1) + 2 * (aquad & 3) + 8 * (aquad >> 3);
+  // Rows past the tile's mini-batches read sample 0 and unit quads past the
+  // block read its first units (both in bounds); stage() masks them to
+  // zero.  The loads are unconditional, so the compiler can wait for one
+  // register set while the next is still in flight.
   const bool alive = arow < rows;
-  const float* asrc = data;
+  const float* asrc = data + kb + 4 * aq;
   if (alive) {
     const int t = e0 * kBatch + arow;  // workspace row: entry e0 + arow / 32, row arow % 32
     int32_t v;
@@ -173,10 +184,14 @@ __global__ void __launch_bounds__(512)
     }
     asrc = data + (int64_t)v * d.d_in + kb + 4 * aq;
   }
-  // W1 staging: k rows 4 wa .. +3, units 4 wq .. +3
-  const int wa = tid >> 5, wq = tid & 31;
+  // W1 staging: k rows 4 wa .. +3, units 4 wq .. +3; wave w takes the k-quads
+  // 2 w and 2 w + 1, four consecutive lanes read 64 contiguous bytes of one k
+  // row, and each load of the wave reads two whole 512-byte row pieces.
+  const int wa = 2 * wave + ((lane >> 2) & 1), wq = 4 * (lane >> 3) + (lane & 3);
   const bool wlive = 4 * wq < units;
-  const float* wsrc = prm + (int64_t)(kb + 4 * wa) * H + u0 + 4 * wq;
+  const float* wsrc = prm + (int64_t)(kb + 4 * wa) * H + u0 + 4 * (wlive ? wq : 0);
+  // masks rather than selects, so the staging has no branches either
+  const uint32_t amask = alive ? ~0u : 0u, wmask = wlive ? ~0u : 0u;
 
   struct Regs {
     f32x4 a[4], w[4];
@@ -184,25 +199,24 @@ __global__ void __launch_bounds__(512)
   auto load = [&](Regs& R, int c) {
     const int k0 = c * kSkKc;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      R.a[j] = alive ? *reinterpret_cast<const f32x4*>(asrc + k0 + 16 * j) : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) R.a[j] = *reinterpret_cast<const f32x4*>(asrc + k0 + 16 * j);
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      R.w[r] = wlive ? *reinterpret_cast<const f32x4*>(wsrc + (int64_t)(k0 + r) * H)
-                     : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int r = 0; r < 4; ++r) R.w[r] = *reinterpret_cast<const f32x4*>(wsrc + (int64_t)(k0 + r) * H);
   };
   auto stage = [&](const Regs& R, int buf) {
-    __bf16* a = As[buf] + arow * kSkLd + 4 * aq;
+    // k-quad aq + 4 j is half aq % 2 of octet aq / 2 + 2 j
+    __bf16* a = As[buf] + arow * kSkLdA + 4 * (aq & 1);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint2 v = {pack_bf16(R.a[j][0], R.a[j][1]), pack_bf16(R.a[j][2], R.a[j][3])};
-      *reinterpret_cast<uint2*>(a + 16 * j) = v;
+      const uint2 v = {pack_bf16(R.a[j][0], R.a[j][1]) & amask, pack_bf16(R.a[j][2], R.a[j][3]) & amask};
+      *reinterpret_cast<uint2*>(a + 8 * (((aq >> 1) + 2 * j) ^ (arow & 7))) = v;
     }
-    __bf16* w = Ws[buf] + (4 * wq) * kSkLd + 4 * wa;
+    // units 4 wq + t, k-quad wa: half wa % 2 of octet wa / 2, swizzled by wq % 8
+    __bf16* w = Ws[buf] + (4 * wq) * kSkLdW + 8 * ((wa >> 1) ^ (wq & 7)) + 4 * (wa & 1);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const uint2 v = {pack_bf16(R.w[0][t], R.w[1][t]), pack_bf16(R.w[2][t], R.w[3][t])};
-      *reinterpret_cast<uint2*>(w + t * kSkLd) = v;
+      const uint2 v = {pack_bf16(R.w[0][t], R.w[1][t]) & wmask, pack_bf16(R.w[2][t], R.w[3][t]) & wmask};
+      *reinterpret_cast<uint2*>(w + t * kSkLdW) = v;
     }
   };
   f32x4 acc[2][4];
@@ -212,28 +226,34 @@ __global__ void __launch_bounds__(512)
     for (int u = 0; u < 4; ++u) acc[f][u] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto multiply = [&](int buf) {
     if (!mma) return;
-    const __bf16* a = As[buf] + (32 * wr + (lane & 15)) * kSkLd + 8 * (lane >> 4);
-    const __bf16* w = Ws[buf] + (64 * wu + (lane & 15)) * kSkLd + 8 * (lane >> 4);
+    // lane: row or unit l % 16 of the fragment, octet 4 ks + l / 16 (swizzled)
+    const int g = lane >> 4;
+    const __bf16* a = As[buf] + (32 * wr + (lane & 15)) * kSkLdA;
+    const __bf16* w = Ws[buf] + (64 * wu + (lane & 15)) * kSkLdW;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
+      const int oa = 8 * ((4 * ks + g) ^ (lane & 7));
       bf16x8 fa[2];
 #pragma unroll
-      for (int f = 0; f < 2; ++f) fa[f] = *reinterpret_cast<const bf16x8*>(a + 16 * f * kSkLd + 32 * ks);
+      for (int f = 0; f < 2; ++f)
+        fa[f] = *reinterpret_cast<const bf16x8*>(a + 16 * f * kSkLdA + oa);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const bf16x8 fb = *reinterpret_cast<const bf16x8*>(w + 16 * u * kSkLd + 32 * ks);
+        const int ow = 8 * ((4 * ks + g) ^ (4 * (u & 1) + ((lane >> 2) & 3)));
+        const bf16x8 fb = *reinterpret_cast<const bf16x8*>(w + 16 * u * kSkLdW + ow);
 #pragma unroll
         for (int f = 0; f < 2; ++f)
           acc[f][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[f], fb, acc[f][u], 0, 0, 0);
       }
     }
   };
+  // prologue: chunks 0 .. kDepth (indices clamped to the last chunk, so the
+  // loads are unconditional and staging chunk 0 waits for its own loads only)
   Regs R[kDepth];
 #pragma unroll
-  for (int c = 0; c < kDepth; ++c)
-    if (c < nck) load(R[c], c);
+  for (int c = 0; c < kDepth; ++c) load(R[c], min(c, nck - 1));
   stage(R[0], 0);
-  if (kDepth < nck) load(R[0], kDepth);
+  load(R[0], min(kDepth, nck - 1));
   __syncthreads();
   // step c: multiply chunk c (buffer c % 2); stage chunk c+1 from its register
   // set and refill that set with chunk c+1+kDepth
@@ -243,7 +263,18 @@ __global__ void __launch_bounds__(512)
     if (c + 1 + kDepth < nck) load(Rn, c + 1 + kDepth);
     __syncthreads();
   };
-  for (int c = 0; c < nck; c += kDepth) {
+  // steady state, branch-free: every step stages and refills its register set
+  int c = 0;
+  for (; c + 2 * kDepth < nck; c += kDepth) {
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j) {
+      multiply((c + j) & 1);
+      stage(R[(j + 1) % kDepth], (c + j + 1) & 1);
+      load(R[(j + 1) % kDepth], c + j + 1 + kDepth);
+      __syncthreads();
+    }
+  }
+  for (; c < nck; c += kDepth) {
 #pragma unroll
     for (int j = 0; j < kDepth; ++j)
       if (c + j < nck) step(c + j, R[(j + 1) % kDepth]);
