@@ -105,8 +105,8 @@ __global__ void __launch_bounds__(256) k_put_idx(int32_t* __restrict__ dst, IdxC
 // are staged through LDS in bf16 ([row][k] and [unit][k]), so a 16-byte read
 // is one MFMA fragment; the 16-byte k-octets of a row are XOR-swizzled so
 // that the fragment reads and the staging writes are free of bank conflicts
-// (A: 64 bf16 per row, octet o at o ^ (row % 8); W1: 80 bf16 per row, octet o
-// at o ^ (unit / 4 % 8); both measured at one LDS cycle per 256 bytes).  Eight waves: wave w takes rows
+// on gfx950 (A: 64 bf16 per row, octet o at o ^ (row % 8); W1: 80 bf16 per
+// row, octet o at o ^ (unit / 4 % 8)).  Eight waves: wave w takes rows
 // 32 (w % 4) .. +31 and units 64 (w / 4) .. +63 (2 x 4 accumulators).  The
 // partial sums go to slice s of the partial buffer; k_mlp_head adds the
 // slices in slice order.  The work items are split into eight equal ranges,
