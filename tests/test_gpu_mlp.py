@@ -69,9 +69,12 @@ def test_grad_small_shape_every_entry(tiny):
 
 
 @pytest.mark.parametrize("d_in,hidden,classes", [(384, 192, 10), (640, 320, 16), (256, 512, 2),
-                                                  (128, 64, 16)])
+                                                  (128, 64, 16), (768, 128, 10), (1024, 64, 5)])
 def test_grad_and_loss_odd_shapes_every_entry(d_in, hidden, classes):
-    """Shapes whose d_in splits into 3 or 2 slices (d_in / 64 = 6 or 10) and
+    """Shapes whose d_in splits into 3 or 2 slices (d_in / 64 = 6 or 10), or
+    into four slices of 1, 3 or 4 chunks of 64 (d_in = 256, 768, 1024: the
+    forward's pipeline tail alone; d_in = 640 and the full shape also run its
+    steady loop), and
     whose hidden units leave a half-filled 128-unit block (192, 320), two and
     sixteen classes; three learners with 1-5 finished mini-batches each, so
     the forward's 4-mini-batch groups come in every size; every finished
