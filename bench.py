@@ -140,6 +140,20 @@ def cpu_baseline_mlp(wl, A, y, x0, budget_s: float = 15.0):
                       f"evaluations not timed)"}
 
 
+def calibration_copy(dev):
+    """One plain 1 GiB device copy (torch's copy kernel), so hardware byte
+    counters taken over the run can be scaled against known bytes."""
+    import torch
+
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    torch.cuda.empty_cache()
+
+
 def bench_mlp(args):
     """End-to-end MLP workload: per iteration the schedule, the shuffled
     indices, the per-mini-batch gradients on the matrix cores and the fused
@@ -205,8 +219,15 @@ def bench_mlp(args):
                      "note": "the fused step, the iteration's largest kernel; events around it "
                              "in the split pass"},
         "eval_loss_after": loss}
+    tr = measured_traffic(wl)
+    if tr is not None:
+        out["roofline"]["traffic"] = tr["traffic_bytes_per_launch"]
+        out["roofline"]["traffic_over_alg"] = tr["traffic_over_alg"]
+        out["roofline"]["traffic_dispatches"] = f"{tr['dispatches']} launches, steps {tr['steps']}"
     del r
     torch.cuda.empty_cache()
+    if args.calibration_copy:
+        calibration_copy(dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_mlp(wl, A, y, x0, args.cpu_budget)
     print(json.dumps(out), flush=True)
@@ -519,13 +540,7 @@ def main():
     }
     out["copy_context"] = copy_context(int(head["roofline"]["alg_bytes_per_launch_mean"]) // 2, dev)
     if args.calibration_copy:
-        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-        torch.cuda.empty_cache()
+        calibration_copy(dev)
     also = args.also
     if also is None:
         also = "resnet18,resnet50" if wl.name == workloads.VGG16_ALLREDUCE.name else "none"
