@@ -352,6 +352,39 @@ def test_full_size_workload_sampled_columns(name):
     assert rel_err(Xg, Xo) <= TOL
 
 
+def test_full_size_server_step_sampled_columns():
+    """Alg. 3's server form at the VGG-16-sized shape, in the launch
+    configuration `bench.py --server` times (row 0 of X as the server model,
+    V and G as allocated there), every iteration of the workload; sampled
+    column windows against the oracle's parameter-server step, masks from the
+    oracle's own schedule."""
+    wl = workloads.get("vgg16")
+    _say(f"full size server step {wl.name}: n={wl.n} m={wl.m} P={wl.P} steps={wl.steps}")
+    r = runner.StepRunner(wl, DEV)
+    counts = []
+    for k in range(wl.steps):
+        mask, c, _, _ = r.plan(k)
+        _lib.step_server(r.Xrows[0], r.Vrows, r.Grows, wl.P, mask, wl.lr, wl.momentum)
+        counts.append(c)
+    torch.cuda.synchronize()
+    cols = _windows(wl.P, 13)
+    idx = torch.from_numpy(cols).to(DEV)
+    xg = r.X[0].index_select(0, idx).cpu().numpy()
+    Vg = r.V.index_select(1, idx).cpu().numpy()
+    del r
+    torch.cuda.empty_cache()
+    X0, G = window_inputs(wl, cols)
+    d = oracle.workload.delay(wl)
+    xo, Vo = X0[0].astype(np.float64), np.zeros((wl.n, len(cols)))
+    lr, mu = float(np.float32(wl.lr)), float(np.float32(wl.momentum))
+    for k in range(wl.steps):
+        mask = oracle.schedule.sample_schedule(wl.seed, k, wl.n, wl.m, d)["mask"]
+        assert np.array_equal(counts[k], mask.sum(axis=1)), k
+        xo, Vo = oracle.step.parameter_server_step(xo, Vo, G, mask, lr, mu)
+    assert rel_err(Vg, Vo) <= TOL
+    assert rel_err(xg, xo) <= TOL
+
+
 def test_gpu_argument_errors():
     n, m, P = 4, 4, 1000
     X = torch.zeros(n * P + 1, dtype=torch.float32, device=DEV)
