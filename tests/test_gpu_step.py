@@ -217,6 +217,51 @@ def test_unfused_stages_and_compositions(n, m, P):
         assert rel_err(Xd.cpu().numpy(), Xo) <= TOL
 
 
+@pytest.mark.parametrize("name", ["resnet18", "resnet50"])
+def test_full_size_unfused_composition_sampled_columns(name):
+    """The three unfused calls composed as `bench.py --unfused` composes them
+    (accumulate, mix, update: the workload's mix-then-step order) at full
+    size on contiguous [n][P] buffers, every iteration of the workload;
+    sampled column windows against the oracle, whose masks come from its own
+    schedule."""
+    from synth import device as synth_device
+
+    wl = workloads.get(name)
+    assert wl.order == "mix_then_step"
+    n, m, P = wl.n, wl.m, wl.P
+    _say(f"full size unfused {wl.name}: n={n} m={m} P={P} steps={wl.steps}")
+    X = torch.empty((n, P), dtype=torch.float32, device=DEV)
+    Y = torch.empty_like(X)
+    V = torch.zeros_like(X)
+    Gbar = torch.empty_like(X)
+    G = torch.empty((n, m, P), dtype=torch.float32, device=DEV)
+    synth_device.fill_normal(X, wl.seed, workloads.STREAM_X, wl.x_std)
+    synth_device.fill_normal(G, wl.seed, workloads.STREAM_G, wl.g_std)
+    sched = runner.Schedule(wl)
+    mixer = runner.Mixer(wl.mixing, n, wl.seed, wl.matcha_degree, wl.matcha_budget)
+    counts = []
+    for k in range(wl.steps):
+        mask, c, _, _ = sched.mask(k)
+        nb.accumulate(G, mask, Gbar)
+        nb.mix(X, mixer.w(k), Y)
+        nb.update(Y, V, Gbar, c, m, wl.lr, wl.momentum)
+        X, Y = Y, X
+        counts.append(c)
+    torch.cuda.synchronize()
+    cols = _windows(P, 17)
+    idx = torch.from_numpy(cols).to(DEV)
+    Xg = X.index_select(1, idx).cpu().numpy()
+    Vg = V.index_select(1, idx).cpu().numpy()
+    del X, Y, V, Gbar, G
+    torch.cuda.empty_cache()
+    X0, Gw = window_inputs(wl, cols)
+    Xo, Vo, masks = oracle_run(wl, X0, Gw, wl.steps)
+    for k in range(wl.steps):
+        assert np.array_equal(counts[k], masks[k].sum(axis=1)), k
+    assert rel_err(Vg, Vo) <= TOL
+    assert rel_err(Xg, Xo) <= TOL
+
+
 def test_mix_in_place_and_uniform_rows_identical():
     n, P = 8, 70001
     rng = np.random.default_rng(1)
