@@ -1,9 +1,10 @@
-/* nbsgd_step_strided called from plain C on device buffers from the HIP
- * runtime: reads one step's inputs from a file, runs the fused step on rows
- * `ld` floats apart whose padding holds a sentinel, checks that the padding
- * is untouched and that misaligned and overlapping buffers are rejected
- * before any launch, and writes X and V (unpadded) to a file.  Used by
- * tests/test_gpu_c_abi.py, which compares them with the oracle.
+/* nbsgd_step_strided (order 0 or 1) or nbsgd_step_server (order 2, with row 0
+ * of X as the server model and W unused) called from plain C on device
+ * buffers from the HIP runtime: reads one step's inputs from a file, runs the
+ * fused step on rows `ld` floats apart whose padding holds a sentinel, checks
+ * that the padding is untouched and that misaligned and overlapping buffers
+ * are rejected before any launch, and writes X and V (unpadded) to a file.
+ * Used by tests/test_gpu_c_abi.py, which compares them with the oracle.
  *
  * Input, little-endian: int32 n, m, order; int64 P, ld; float lr, momentum;
  * uint8 mask[n*m]; float W[n*n], X[n*P], V[n*P], G[n*m*P].
@@ -83,21 +84,28 @@ int main(int argc, char **argv) {
     return 3;
 
   int failures = 0;
+  const int server = order == 2;
   /* rejected before any launch: a misaligned base and X overlapping V */
-  if (nbsgd_step_strided(dX + 1, dV, dG, ld, mask, W, n, m, P, lr, momentum, order, NULL) !=
-      NBSGD_E_ALIGN) {
+  const nbsgd_status misaligned =
+      server ? nbsgd_step_server(dX + 1, dV, dG, ld, mask, n, m, P, lr, momentum, NULL)
+             : nbsgd_step_strided(dX + 1, dV, dG, ld, mask, W, n, m, P, lr, momentum, order, NULL);
+  if (misaligned != NBSGD_E_ALIGN) {
     fprintf(stderr, "misaligned X was not rejected\n");
     ++failures;
   }
-  if (nbsgd_step_strided(dX, dX, dG, ld, mask, W, n, m, P, lr, momentum, order, NULL) !=
-      NBSGD_E_ARG) {
+  const nbsgd_status overlap =
+      server ? nbsgd_step_server(dX, dX, dG, ld, mask, n, m, P, lr, momentum, NULL)
+             : nbsgd_step_strided(dX, dX, dG, ld, mask, W, n, m, P, lr, momentum, order, NULL);
+  if (overlap != NBSGD_E_ARG) {
     fprintf(stderr, "X overlapping V was not rejected\n");
     ++failures;
   }
   const nbsgd_status st =
-      nbsgd_step_strided(dX, dV, dG, ld, mask, W, n, m, P, lr, momentum, order, NULL);
+      server ? nbsgd_step_server(dX, dV, dG, ld, mask, n, m, P, lr, momentum, NULL)
+             : nbsgd_step_strided(dX, dV, dG, ld, mask, W, n, m, P, lr, momentum, order, NULL);
   if (st != NBSGD_OK) {
-    fprintf(stderr, "nbsgd_step_strided: status %d: %s\n", (int)st, nbsgd_last_error());
+    fprintf(stderr, "%s: status %d: %s\n", server ? "nbsgd_step_server" : "nbsgd_step_strided",
+            (int)st, nbsgd_last_error());
     return 4;
   }
   if (!hip_ok(hipDeviceSynchronize(), "hipDeviceSynchronize")) return 3;
